@@ -1,0 +1,277 @@
+#!/usr/bin/env python3
+"""Benchmark of the chunked MoE expert layer on one MI355X.
+
+One step = one pass of the whole hot path over one batch of received tokens:
+expert counts (the paper's "first notification") -> memory-aware chunk plan
+(Eq. (8)/(9) + bins) -> chunked forward (Eq. (6)) -> chunked-recompute
+backward (Eq. (7)).  Inputs are synthetic, seeded, and resident in HBM before
+the timed region starts.
+
+Prints ONE JSON line (rank 0, N = 1 GPU):
+  value        received tokens per second (whole job = one GPU)
+  roofline     the dominant kernel's algorithmic TFLOP/s against the bf16
+               MFMA peak, measured with HIP events inside the timed region
+  cpu_baseline the fp64 oracle on the host cores, on a bounded token sample
+  chunks_sweep tokens/s and measured peak activation bytes for every chunk
+               count of the workload, beside the memory-model predictions
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+HBM_GBS = 8000.0
+
+# activation budget handed to the planner per workload (bytes); the plan
+# then picks C from the bins
+DEFAULT_BUDGET = {1: 64 * 1024, 2: 250 * 10**6, 3: 500 * 10**6, 4: 10**9, 5: 8 * 10**9}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2, help="workload number (1-5)")
+    ap.add_argument("--budget", type=float, default=None, help="activation budget, bytes")
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target duration of the oracle sample")
+    return ap.parse_args()
+
+
+def source_digest(kernel_file: str) -> str:
+    path = os.path.join(ROOT, "paper_2511_21431_amd", "csrc", kernel_file)
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def read_traffic(kernel: str, workload: str):
+    """HBM bytes per launch measured with rocprofv3 counters, if a summary for
+    this kernel and workload exists and the kernel source has not changed
+    since (the summary records the source digest)."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        with open(path) as f:
+            d = json.load(f)
+        if d.get("source_sha256_16") != source_digest(d.get("source", "grouped_gemm.hip")):
+            return None
+        return float(d["bytes_per_launch"])
+    except Exception:
+        return None
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(the expert-parallel exchange is out of scope), so --gpus must be 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import moe_workloads as mw
+    import paper_2511_21431_amd as mf
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    mf.lib()
+
+    cfg = args.config
+    w = mw.WORKLOADS[cfg]
+    seed = cfg if args.seed is None else args.seed
+    budget = int(args.budget) if args.budget is not None else DEFAULT_BUDGET[cfg]
+    bins = w.bins
+    dtype = mf.BF16 if w.dtype == "bf16" else mf.F32
+    shape = mf.make_shape(w.T, w.h, w.F, w.E, w.k, dtype)
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+
+    log(f"[bench] workload {cfg} {w.name}: T={w.T} h={w.h} F={w.F} E={w.E} k={w.k} {w.dtype}")
+    idx_np, gates_np = mw.make_routing(w, seed)
+    dev = mw.make_tensors_device(w, seed, "cuda")
+    idx = torch.from_numpy(idx_np).cuda()
+    gates = torch.from_numpy(gates_np).cuda()
+    Y = torch.empty((w.T, w.h), dtype=dt, device="cuda")
+    dX = torch.empty_like(Y)
+    dW1 = torch.empty((w.E, 2 * w.F, w.h), dtype=torch.float32, device="cuda")
+    dW2 = torch.empty((w.E, w.h, w.F), dtype=torch.float32, device="cuda")
+    dg = torch.empty((w.T, w.k), dtype=torch.float32, device="cuda")
+    work = torch.zeros(w.E + 1, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+
+    def step(C_fixed=None, allocator=None):
+        counts = mf.memfine_count(shape, idx, work)            # syncs once
+        rc, C, info = mf.memfine_plan(shape, counts, budget, bins=bins)
+        if C_fixed is not None:
+            C = C_fixed
+        mf.memfine_moe_fwd(shape, C, dev["X"], idx, gates, dev["W1"], dev["W2"], Y,
+                           allocator=allocator)
+        mf.memfine_moe_bwd(shape, C, dev["X"], idx, gates, dev["W1"], dev["W2"], dev["dY"], dX,
+                           dW1, dW2, dg, allocator=allocator)
+        return C, info
+
+    # ---- warm-up, and one fully instrumented step to find the dominant kernel
+    for _ in range(max(args.warmup, 1)):
+        C, plan_info = step()
+    torch.cuda.synchronize()
+    mf.memfine_profile_begin()
+    step()
+    torch.cuda.synchronize()
+    prof_all = mf.memfine_profile_end()
+    dominant = max(prof_all, key=lambda k: prof_all[k]["total_ms"])
+    log(f"[bench] plan: C={C} (c_theory={plan_info['c_theory']}, s''={plan_info['s_recv']}, "
+        f"budget={budget}); dominant kernel: {dominant}")
+    for k, v in sorted(prof_all.items(), key=lambda kv: -kv[1]["total_ms"]):
+        log(f"[bench]   {k:14s} {v['launches']:3d} launches {v['total_ms']:8.3f} ms "
+            f"{v['flops'] / max(v['total_ms'], 1e-9) / 1e9:8.1f} TFLOP/s "
+            f"{v['bytes'] / max(v['total_ms'], 1e-9) / 1e6:8.1f} GB/s")
+
+    # ---- timed region
+    mf.memfine_profile_begin([dominant])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = mf.memfine_profile_end()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    tokens_per_s = w.T * args.steps / (t1 - t0)
+    d = prof[dominant]
+    avg_ms = d["total_ms"] / d["launches"]
+    flops_per_launch = d["flops"] / d["launches"]
+    achieved = flops_per_launch / (avg_ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[w.dtype]
+    traffic = read_traffic(dominant, f"cfg{cfg}")
+    executed_flops = 22.0 * w.N * w.h * w.F
+    log(f"[bench] {ms_per_step:.3f} ms/step, {tokens_per_s:.0f} tokens/s, dominant {dominant} "
+        f"avg {avg_ms:.3f} ms {achieved:.1f} TFLOP/s")
+
+    # ---- chunk-count sweep: throughput and measured peak activation memory
+    sweep = []
+    if not args.no_sweep:
+        for Cs in w.chunks:
+            for _ in range(2):
+                step(Cs)
+            torch.cuda.synchronize()
+            n_t = max(3, args.steps // 4)
+            a = time.perf_counter()
+            for _ in range(n_t):
+                step(Cs)
+            torch.cuda.synchronize()
+            tps = w.T * n_t / (time.perf_counter() - a)
+            alloc = mf.TorchAllocator()
+            torch.cuda.synchronize()
+            torch.cuda.reset_peak_memory_stats()
+            base = torch.cuda.memory_allocated()
+            step(Cs, allocator=alloc)
+            torch.cuda.synchronize()
+            peak_b = torch.cuda.max_memory_allocated() - base
+            n_max = -(-w.T // Cs) * w.k
+            beta_paper = (2 if w.dtype == "bf16" else 4) * (2 * w.h + 2 * w.F)
+            sweep.append({
+                "chunks": Cs, "tokens_per_s": round(tps, 1),
+                "peak_activation_bytes": int(peak_b),
+                "allocator_high_water_bytes": int(alloc.high_water),
+                "predicted_bytes_impl": mf.memfine_workspace_bytes(shape, Cs, mf.PASS_BWD),
+                "predicted_bytes_paper_model": beta_paper * n_max,
+            })
+            log(f"[bench] sweep C={Cs}: {tps:.0f} tokens/s, peak activation {peak_b / 1e9:.3f} GB")
+
+    # ---- the oracle on the host cores, bounded sample of the same workload
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, idx_np, gates_np, dev, C, args.cpu_seconds)
+
+    out = {
+        "metric": "chunked MoE layer fwd+bwd tokens/sec on 1 GPU",
+        "value": round(tokens_per_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded routing and N(0,1)/N(0,0.02) tensors)",
+        "config": {"workload": f"{w.name}: T={w.T} received tokens, h={w.h}, F={w.F}, "
+                               f"E={w.E} local experts, top-{w.k}",
+                   "T": w.T, "h": w.h, "F": w.F, "E": w.E, "k": w.k,
+                   "chunks": C, "budget_bytes": budget, "bins": list(bins),
+                   "parallelism": "single GPU (one expert-parallel share)"},
+        "mfma_util_layer": round(executed_flops / (ms_per_step * 1e-3) / 1e12 / peak, 4),
+        "layer_tflops": round(executed_flops / (ms_per_step * 1e-3) / 1e12, 1),
+        "roofline": {"kernel": dominant, "bound": "mfma", "achieved": round(achieved, 1),
+                     "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                     "traffic": traffic, "avg_launch_ms": round(avg_ms, 4),
+                     "launches": d["launches"], "flops_per_launch": flops_per_launch},
+        "kernels_one_step": {k: {"ms": round(v["total_ms"], 4),
+                                 "tflops": round(v["flops"] / max(v["total_ms"], 1e-9) / 1e9, 1),
+                                 "gbs": round(v["bytes"] / max(v["total_ms"], 1e-9) / 1e6, 1)}
+                             for k, v in prof_all.items()},
+        "chunks_sweep": sweep,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, idx_np, gates_np, dev, C, target_s):
+    """The oracle, as it stands, on the host: fp64 fwd + chunked-recompute bwd
+    over the first T_s tokens (same weights, same chunk count)."""
+    import torch
+
+    from oracle import moe as om
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    log("[bench] cpu baseline: copying weights to host")
+    W1 = dev["W1"].double().cpu().numpy()
+    W2 = dev["W2"].double().cpu().numpy()
+    Ts = max(16, min(w.T, 256))
+    elapsed = 0.0
+    while True:
+        X = dev["X"][:Ts].double().cpu().numpy()
+        dY = dev["dY"][:Ts].double().cpu().numpy()
+        a = time.perf_counter()
+        om.moe_fwd(X, idx_np[:Ts], gates_np[:Ts], W1, W2, C)
+        om.moe_bwd(X, idx_np[:Ts], gates_np[:Ts], W1, W2, dY, C)
+        elapsed = time.perf_counter() - a
+        log(f"[bench] cpu baseline: {Ts} tokens in {elapsed:.2f} s")
+        if elapsed >= target_s / 3 or Ts >= w.T:
+            break
+        Ts = min(w.T, int(Ts * max(2.0, target_s / max(elapsed, 1e-3))))
+    del W1, W2
+    torch.cuda.synchronize()
+    return {"value": round(Ts / elapsed, 2), "unit": "tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"first {Ts} of {w.T} tokens, fp64 NumPy oracle fwd + chunked-recompute "
+                      f"bwd at C={C}, {elapsed:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

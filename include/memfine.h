@@ -1,0 +1,225 @@
+/*
+ * memfine.h - C ABI of the MI355X (gfx950) chunked MoE expert layer.
+ *
+ * The layer is the per-GPU hot path of MemFine (memory-aware fine-grained
+ * scheduling for MoE training): on one GPU's share of expert-parallel work it
+ * runs dispatch (group the received token-slots by local expert), the expert
+ * SwiGLU FFN on every expert's rows, and the gate-weighted combine, over C
+ * contiguous token chunks (paper Section 4.1, Eq. (6)); the backward
+ * recomputes each chunk before back-propagating it (Eq. (7)).  C comes from
+ * the paper's activation-memory model (Section 4.2, Eq. (8), Eq. (9), bins).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers named d_* are device pointers, h_* host pointers.  Every buffer
+ *   is owned by the caller; the library keeps no state between calls except a
+ *   lazily created per-process profiling table.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *   Device work is enqueued asynchronously on it; only memfine_count and
+ *   memfine_profile_end synchronise (with the stream / the recorded events).
+ * - Return value: MEMFINE_OK (0) or a negative status.  Argument errors are
+ *   detected on the host and returned before anything is enqueued.  A HIP
+ *   failure returns MEMFINE_ERR_HIP; an allocator that returns NULL gives
+ *   MEMFINE_ERR_OOM.  After a failed call the outputs are unspecified, and
+ *   every internal allocation has been handed back.
+ * - Shapes (memfine_shape): T received tokens, h hidden size, F expert FFN
+ *   size (g_e in the paper), E local experts, k slots per token (top-k).
+ *   Requirements: T >= 0, T*k < 2^31, h % 64 == 0, F % 64 == 0, h, F >= 64,
+ *   1 <= k, 1 <= E <= 1024.
+ * - Layouts, all row-major and contiguous:
+ *     idx    int32 [T, k]       expert of each slot, 0 <= idx < E
+ *     gates  float [T, k]       score of each slot (need not sum to 1)
+ *     X, Y, dY, dX   dtype [T, h]
+ *     W1     dtype [E, 2F, h]   rows 0..F-1: SiLU gate, rows F..2F-1: up
+ *     W2     dtype [E, h, F]
+ *     dW1, dW2  float, shaped like W1, W2;   dgates float [T, k]
+ *   dtype is bf16 (MEMFINE_BF16, raw 16-bit storage) or float (MEMFINE_F32).
+ *   Per slot (token t, slot j, expert e = idx[t,j], g = gates[t,j]):
+ *     u = W1[e] X[t];  a = silu(u[0:F]) * u[F:2F];  Y[t] += g * (W2[e] a).
+ *   Arithmetic: fp32 accumulation everywhere; on the bf16 path the per-chunk
+ *   intermediates are stored as bf16.
+ */
+#ifndef MEMFINE_H
+#define MEMFINE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define MEMFINE_OK                0
+#define MEMFINE_ERR_INVALID_ARG  (-1)
+#define MEMFINE_ERR_UNSUPPORTED  (-2)
+#define MEMFINE_ERR_BUDGET       (-3)
+#define MEMFINE_ERR_OOM          (-4)
+#define MEMFINE_ERR_HIP          (-5)
+
+/* element types */
+#define MEMFINE_BF16  0
+#define MEMFINE_F32   1
+
+/* passes for memfine_workspace_bytes */
+#define MEMFINE_PASS_FWD  0
+#define MEMFINE_PASS_BWD  1
+
+typedef struct memfine_shape {
+  int64_t T;      /* received tokens (rows of X)                       */
+  int32_t h;      /* hidden size                                        */
+  int32_t F;      /* expert FFN size (SwiGLU width; FC1 has 2F rows)    */
+  int32_t E;      /* local experts                                      */
+  int32_t k;      /* slots per token (top-k)                            */
+  int32_t dtype;  /* MEMFINE_BF16 or MEMFINE_F32                        */
+} memfine_shape;
+
+/*
+ * Optional device-memory provider for the per-chunk working buffers.
+ * alloc(bytes, stream, ctx) returns a device pointer (256-byte aligned) that
+ * is usable in stream order on `stream`, or NULL on failure; release(ptr,
+ * bytes, stream, ctx) gives it back in stream order.  When the allocator
+ * argument of a call is NULL the library uses hipMallocAsync/hipFreeAsync on
+ * the call's stream.
+ */
+typedef struct memfine_allocator {
+  void* (*alloc)(size_t bytes, void* stream, void* ctx);
+  void (*release)(void* ptr, size_t bytes, void* stream, void* ctx);
+  void* ctx;
+} memfine_allocator;
+
+/* Output of the planner (all fields filled on MEMFINE_OK and on
+ * MEMFINE_ERR_BUDGET). */
+typedef struct memfine_plan_info {
+  int64_t s_recv;        /* s'': received slots, the sum of the counts      */
+  int64_t beta;          /* bytes per received slot used by the plan        */
+  int64_t avail;         /* budget - fixed, the numerator of Eq. (8)        */
+  double s_max;          /* Eq. (8): avail / beta (for reporting only)      */
+  int64_t c_theory;      /* Eq. (9): ceil(s'' / s'_max); -1 if avail <= 0   */
+  int32_t chunks;        /* chosen chunk count (a bin)                      */
+  int32_t fits;          /* 1 if chunks >= c_theory                         */
+  int64_t paper_peak_bytes; /* beta * slots of the largest chunk            */
+} memfine_plan_info;
+
+/*
+ * Expert counts over all T tokens: the "first notification" of the paper's
+ * Section 4.2 that delivers the number of received slots s''.
+ *   d_idx     int32 [T, k] device
+ *   d_work    int32 [E + 1] device scratch owned by the caller; on return
+ *             d_work[e] = slots routed to expert e and d_work[E] = number of
+ *             ids outside [0, E)
+ *   h_counts  int64 [E] host output
+ * Synchronises `stream`.  Returns MEMFINE_ERR_INVALID_ARG when any id is out
+ * of range (h_counts then counts only the valid ids).
+ */
+int memfine_count(const memfine_shape* shape, const int32_t* d_idx, int32_t* d_work,
+                  int64_t* h_counts, void* stream);
+
+/*
+ * Dispatch of one chunk, tokens [t0, t1) (the "dispatch" of Eq. (4)), exposed
+ * so that tests can check the exact permutation the layer uses.  With
+ * n = (t1 - t0) * k and global slot id s = t * k + j:
+ *   d_counts       int32 [E]       slots of expert e in the chunk
+ *   d_offsets      int32 [E + 1]   exclusive prefix sum, d_offsets[E] = n
+ *   d_sorted_slot  int32 [n]       slot ids grouped by expert; ascending
+ *                                  slot id inside an expert (stable)
+ *   d_row_of_slot  int32 [n]       row of slot t0*k + i in that order
+ * Precondition: ids already validated (memfine_count).  Scratch comes from
+ * `alloc` (NULL = hipMallocAsync).  Asynchronous.
+ */
+int memfine_dispatch(const memfine_shape* shape, const int32_t* d_idx, int64_t t0, int64_t t1,
+                     int32_t* d_counts, int32_t* d_offsets, int32_t* d_sorted_slot,
+                     int32_t* d_row_of_slot, const memfine_allocator* alloc, void* stream);
+
+/*
+ * Memory-aware chunk tuning (paper Section 4.2).  Pure host arithmetic, exact
+ * in integers.
+ *   h_counts      int64 [E]   slots per local expert (memfine_count)
+ *   budget_bytes  the numerator of Eq. (8): memory left for this layer's
+ *                 chunked MoE activations (alpha*M_GPU - M_sta - non-MoE)
+ *   fixed_bytes   subtracted from the budget first (>= 0)
+ *   beta_bytes    bytes per received slot; 0 selects the paper's Table 2
+ *                 rows 11-13, D_t * (2h + 2F)
+ *   bins, nbins   allowed chunk counts (each >= 1), e.g. {1, 2, 4, 8}
+ * Chooses s'' = sum(counts), s'_max = (budget - fixed) / beta (Eq. (8)),
+ * c = ceil(s'' / s'_max) (Eq. (9)), then the smallest bin >= c (decided
+ * exactly as bin * (budget - fixed) >= s'' * beta).  If no bin is large
+ * enough, or budget - fixed <= 0, *chunks_out = the largest bin and the call
+ * returns MEMFINE_ERR_BUDGET.  s'' = 0 gives the smallest bin.  `info` may be
+ * NULL.
+ */
+int memfine_plan(const memfine_shape* shape, const int64_t* h_counts, int64_t budget_bytes,
+                 int64_t fixed_bytes, int64_t beta_bytes, const int32_t* bins, int32_t nbins,
+                 int32_t* chunks_out, memfine_plan_info* info);
+
+/*
+ * Bytes of working memory the layer allocates for its largest chunk (the
+ * per-chunk buffers of memfine_moe_fwd or memfine_moe_bwd, pass =
+ * MEMFINE_PASS_FWD / MEMFINE_PASS_BWD) - the activation peak of the chunked
+ * layer that Section 4.1 says replaces the unchunked one.  Returns < 0 on
+ * invalid arguments.
+ */
+int64_t memfine_workspace_bytes(const memfine_shape* shape, int32_t chunks, int32_t pass);
+
+/*
+ * Chunked forward, Eq. (6): Y = concat(F_w(X_1), ..., F_w(X_C)), with
+ * F_w = combine(expert(dispatch(.))) of Eq. (4) on tokens
+ * [floor(i*T/C), floor((i+1)*T/C)).  Every chunk's buffers are allocated
+ * before and released after its kernels.  Nothing is kept for the backward.
+ * Y is overwritten.  `chunks` >= 1 (chunks > T behaves like T).
+ */
+int memfine_moe_fwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
+                    const int32_t* d_idx, const float* d_gates, const void* d_W1,
+                    const void* d_W2, void* d_Y, const memfine_allocator* alloc, void* stream);
+
+/*
+ * Chunked-recompute backward, Eq. (7): for each chunk in ascending order,
+ * recompute its forward, then back-propagate dY's rows of that chunk.
+ * Overwrites dX and dgates.  dW1/dW2 are overwritten when accumulate_dW == 0
+ * and added to when accumulate_dW == 1.
+ */
+int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
+                    const int32_t* d_idx, const float* d_gates, const void* d_W1,
+                    const void* d_W2, const void* d_dY, void* d_dX, float* d_dW1, float* d_dW2,
+                    float* d_dgates, int32_t accumulate_dW, const memfine_allocator* alloc,
+                    void* stream);
+
+/* Static, human-readable text for a status code. */
+const char* memfine_status_str(int status);
+
+/*
+ * Kernel timing for performance reports.  memfine_profile_begin(mask) makes
+ * later calls record a pair of HIP events around every launch of the kernels
+ * whose id bit is set in `mask` (ids: MEMFINE_K_*).  memfine_profile_end waits
+ * for those events and returns, per kernel id, the number of launches, the
+ * summed launch durations in milliseconds, and the algorithmic flops and HBM
+ * bytes of those launches; then it stops recording.
+ */
+#define MEMFINE_K_COUNT       0
+#define MEMFINE_K_DISPATCH    1
+#define MEMFINE_K_FC1         2   /* forward FC1 + SwiGLU                    */
+#define MEMFINE_K_FC2         3   /* forward FC2                             */
+#define MEMFINE_K_COMBINE     4
+#define MEMFINE_K_FC1_RECOMP  5   /* backward: FC1 recompute (u and g*a)      */
+#define MEMFINE_K_FC2_DGRAD   6   /* dA = dY W2 with fused SwiGLU backward   */
+#define MEMFINE_K_FC2_WGRAD   7
+#define MEMFINE_K_FC1_WGRAD   8
+#define MEMFINE_K_FC1_DGRAD   9
+#define MEMFINE_K_UNPERMUTE  10   /* dX sum over slots and gate gradient     */
+#define MEMFINE_K_NUM        11
+
+typedef struct memfine_kernel_stat {
+  int64_t launches;
+  double total_ms;
+  double flops;   /* algorithmic floating-point operations, all launches */
+  double bytes;   /* algorithmic HBM bytes, all launches                  */
+} memfine_kernel_stat;
+
+int memfine_profile_begin(uint32_t mask);
+int memfine_profile_end(memfine_kernel_stat* out /* [MEMFINE_K_NUM] */);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MEMFINE_H */

@@ -3,8 +3,11 @@
 This module is the only code shared by the fp64 oracle side (tests) and the
 HIP side (tests, bench).  It draws routing and tensors and does nothing of the
 layer's own arithmetic: no dispatch, no expert FFN, no combine, no memory
-model.  Everything is NumPy with a PCG64 generator so that a (config, seed)
-pair always yields the same arrays on every machine.
+model.  Routing is always NumPy (PCG64), so that a (config, seed) pair
+yields the same routing on every machine; tensors come either from NumPy
+(small cases the oracle checks in full) or, for the multi-GB workloads, from
+torch's seeded generator directly in device memory (make_tensors_device), and
+the oracle then reads the slices it needs back to the host.
 
 Workload recipe (the paper's training corpus and trained weights are not
 available; these synthetic draws stand in for the skewed per-GPU token
@@ -191,3 +194,35 @@ def make_case(w: Workload, seed: int, with_dy: bool = True) -> Dict[str, np.ndar
 def scaled(w: Workload, **kw) -> Workload:
     """A copy of ``w`` with other sizes (same routing recipe), for parity runs."""
     return w.with_(**kw)
+
+
+def make_tensors_device(w: Workload, seed: int, device, with_dy: bool = True):
+    """Draw X, W1, W2 (and dY) directly in device memory with torch's seeded
+    generator (for the multi-GB workloads; same distributions as
+    make_tensors, bf16 by round-to-nearest-even).  Returns torch tensors in
+    the workload's storage dtype."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed) * 1000003 + 17)
+    bf16 = w.dtype == "bf16"
+    dt = torch.bfloat16 if bf16 else torch.float32
+    s1, s2 = (0.02, 0.02) if bf16 else (w.h ** -0.5, w.F ** -0.5)
+
+    def normal(shape, std):
+        t = torch.empty(shape, dtype=dt, device=device)
+        # fill in slices to bound the float32 staging buffer
+        flat = t.view(-1)
+        step = 1 << 26
+        for i in range(0, flat.numel(), step):
+            j = min(flat.numel(), i + step)
+            x = torch.randn(j - i, generator=gen, device=device, dtype=torch.float32)
+            if std != 1.0:
+                x.mul_(std)
+            flat[i:j].copy_(x)
+        return t
+
+    out = {"X": normal((w.T, w.h), 1.0), "W1": normal((w.E, 2 * w.F, w.h), s1),
+           "W2": normal((w.E, w.h, w.F), s2)}
+    if with_dy:
+        out["dY"] = normal((w.T, w.h), 1.0)
+    return out

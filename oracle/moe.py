@@ -301,3 +301,26 @@ def moe_dW_expert(X, idx, gates, W1, W2, dY, e: int):
     du = np.concatenate([da * uu * silu_grad(ug), da * silu(ug)], axis=1)
     dW1 = du.T @ x
     return dW1, dW2
+
+
+def moe_dW_expert_columns(X, idx, gates, W1, W2, dY, e: int, fs):
+    """Selected columns f of expert e's weight gradients, each from its
+    definition over the expert's slots: rows f and F+f of dW1[e] and column f
+    of dW2[e].  Returns (dW1_gate [len(fs), h], dW1_up [len(fs), h],
+    dW2_col [h, len(fs)])."""
+    k = idx.shape[1]
+    F = W1.shape[1] // 2
+    fs = np.asarray(list(fs), dtype=np.int64)
+    slots = np.nonzero(np.asarray(idx).reshape(-1) == e)[0]
+    tok = slots // k
+    jj = slots % k
+    x = _f64(X[tok])
+    g = _f64(gates)[tok, jj]
+    dy = _f64(dY[tok])
+    ug = x @ _f64(W1[e][fs]).T                      # [n_e, |fs|]
+    uu = x @ _f64(W1[e][F + fs]).T
+    a = silu(ug) * uu
+    da = g[:, None] * (dy @ _f64(W2[e][:, fs]))     # [n_e, |fs|]
+    du_g = da * uu * silu_grad(ug)
+    du_u = da * silu(ug)
+    return du_g.T @ x, du_u.T @ x, (g[:, None] * dy).T @ a

@@ -1,0 +1,9 @@
+"""MI355X-native chunked MoE expert layer (MemFine's per-GPU hot path).
+
+The compute lives in libmemfine.so (hand-written gfx950 HIP kernels behind
+the C ABI of include/memfine.h); this package only builds and binds it.
+"""
+from ._lib import (BF16, F32, PASS_BWD, PASS_FWD, MemfineError, TorchAllocator,  # noqa: F401
+                   lib, make_shape, memfine_count, memfine_dispatch, memfine_moe_bwd,
+                   memfine_moe_fwd, memfine_plan, memfine_profile_begin, memfine_profile_end,
+                   memfine_status_str, memfine_workspace_bytes)

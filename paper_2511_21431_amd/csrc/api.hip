@@ -1,0 +1,529 @@
+// C ABI of the chunked MoE expert layer: argument checks, the memory-aware
+// chunk planner, the per-chunk workspace layout, and the chunk driver that
+// allocates, fills and releases every chunk's buffers in stream order
+// (paper Section 4.1, Eq. (6)/(7); Section 4.2, Eq. (8)/(9)).
+#include <algorithm>
+#include <mutex>
+#include <unordered_map>
+#include <vector>
+
+#include "kernels.h"
+#include "memfine.h"
+
+using namespace memfine;
+
+namespace {
+
+// ------------------------------------------------------------- profiling
+struct ProfRecord {
+  int id;
+  hipEvent_t start, stop;
+  double flops, bytes;
+};
+std::mutex g_prof_mu;
+uint32_t g_prof_mask = 0;
+std::vector<ProfRecord> g_prof;
+
+class KernelTimer {
+ public:
+  KernelTimer(int id, hipStream_t s, double flops, double bytes)
+      : id_(id), s_(s), flops_(flops), bytes_(bytes) {
+    on_ = (g_prof_mask >> id) & 1u;
+    if (on_) {
+      on_ = hipEventCreate(&a_) == hipSuccess && hipEventCreate(&b_) == hipSuccess &&
+            hipEventRecord(a_, s_) == hipSuccess;
+    }
+  }
+  ~KernelTimer() {
+    if (!on_) return;
+    if (hipEventRecord(b_, s_) != hipSuccess) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof.push_back({id_, a_, b_, flops_, bytes_});
+  }
+
+ private:
+  int id_;
+  hipStream_t s_;
+  double flops_, bytes_;
+  bool on_ = false;
+  hipEvent_t a_ = nullptr, b_ = nullptr;
+};
+
+// ----------------------------------------------------------------- checks
+int check_shape(const memfine_shape* s) {
+  if (!s) return MEMFINE_ERR_INVALID_ARG;
+  if (s->T < 0 || s->h < 64 || s->F < 64 || (s->h % 64) || (s->F % 64) || s->k < 1 || s->E < 1 ||
+      s->E > 1024)
+    return MEMFINE_ERR_INVALID_ARG;
+  if (s->dtype != MEMFINE_BF16 && s->dtype != MEMFINE_F32) return MEMFINE_ERR_UNSUPPORTED;
+  if (s->T * (int64_t)s->k >= (int64_t(1) << 31)) return MEMFINE_ERR_UNSUPPORTED;
+  return MEMFINE_OK;
+}
+
+int64_t elem_bytes(const memfine_shape& s) { return s.dtype == MEMFINE_BF16 ? 2 : 4; }
+
+// ------------------------------------------------------ workspace layout
+// One allocation per chunk, carved into 256-byte aligned buffers.
+struct Layout {
+  enum {
+    kBcount, kBstart, kCounts, kOffsets, kOrder, kSorted, kRowOf, kTokOf, kGateOf,
+    kA, kY,                 // forward
+    kU, kAg, kDxp, kDgp,    // backward
+    kNum
+  };
+  int64_t off[kNum];
+  int64_t size[kNum];
+  int64_t total;
+};
+
+int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+void chunk_layout(const memfine_shape& s, int64_t n, int pass, Layout& L) {
+  const int64_t es = elem_bytes(s), E = s.E, nb = dispatch_blocks(n);
+  const int64_t P = dgate_partials(s.F);
+  for (int i = 0; i < Layout::kNum; ++i) L.size[i] = 0;
+  L.size[Layout::kBcount] = E * nb * 4;
+  L.size[Layout::kBstart] = E * nb * 4;
+  L.size[Layout::kCounts] = E * 4;
+  L.size[Layout::kOffsets] = (E + 1) * 4;
+  L.size[Layout::kOrder] = E * 4;
+  L.size[Layout::kSorted] = n * 4;
+  L.size[Layout::kRowOf] = n * 4;
+  L.size[Layout::kTokOf] = n * 4;
+  L.size[Layout::kGateOf] = n * 4;
+  if (pass == MEMFINE_PASS_FWD) {
+    L.size[Layout::kA] = n * s.F * es;
+    L.size[Layout::kY] = n * s.h * es;
+  } else {
+    L.size[Layout::kU] = n * 2 * s.F * es;
+    L.size[Layout::kAg] = n * s.F * es;
+    L.size[Layout::kDxp] = n * s.h * es;
+    L.size[Layout::kDgp] = n * P * 4;
+  }
+  int64_t o = 0;
+  for (int i = 0; i < Layout::kNum; ++i) {
+    L.off[i] = o;
+    o += align256(L.size[i]);
+  }
+  L.total = o;
+}
+
+// tokens in the largest chunk of the floor-balanced split of T into C
+int64_t max_chunk_tokens(int64_t T, int64_t C) {
+  if (T == 0) return 0;
+  C = std::min(C, T);
+  return (T + C - 1) / C;
+}
+
+// --------------------------------------------------------------- memory
+std::mutex g_pool_mu;
+std::unordered_map<int, hipMemPool_t> g_pools;
+
+// A private stream-ordered pool per device that keeps freed memory cached,
+// so releasing a chunk's buffers and allocating the next chunk's reuses the
+// same memory without a trip to the driver.
+hipMemPool_t device_pool() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  std::lock_guard<std::mutex> lk(g_pool_mu);
+  auto it = g_pools.find(dev);
+  if (it != g_pools.end()) return it->second;
+  hipMemPoolProps props = {};
+  props.allocType = hipMemAllocationTypePinned;
+  props.location.type = hipMemLocationTypeDevice;
+  props.location.id = dev;
+  hipMemPool_t pool = nullptr;
+  if (hipMemPoolCreate(&pool, &props) != hipSuccess) return nullptr;
+  uint64_t keep = UINT64_MAX;
+  hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+  g_pools[dev] = pool;
+  return pool;
+}
+
+void* ws_alloc(const memfine_allocator* a, size_t bytes, hipStream_t s) {
+  if (bytes == 0) bytes = 256;
+  if (a && a->alloc) return a->alloc(bytes, (void*)s, a->ctx);
+  hipMemPool_t pool = device_pool();
+  if (!pool) return nullptr;
+  void* p = nullptr;
+  if (hipMallocFromPoolAsync(&p, bytes, pool, s) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  return p;
+}
+
+void ws_release(const memfine_allocator* a, void* p, size_t bytes, hipStream_t s) {
+  if (!p) return;
+  if (bytes == 0) bytes = 256;
+  if (a && a->release) a->release(p, bytes, (void*)s, a->ctx);
+  else if (!(a && a->alloc)) (void)hipFreeAsync(p, s);
+}
+
+struct ChunkBuffers {
+  ChunkMeta m;
+  void *a, *y, *u, *ag, *dxp;
+  float* dgp;
+};
+
+ChunkBuffers carve(void* base, const Layout& L) {
+  char* b = (char*)base;
+  ChunkBuffers c;
+  c.m.bcount = (int32_t*)(b + L.off[Layout::kBcount]);
+  c.m.bstart = (int32_t*)(b + L.off[Layout::kBstart]);
+  c.m.counts = (int32_t*)(b + L.off[Layout::kCounts]);
+  c.m.offsets = (int32_t*)(b + L.off[Layout::kOffsets]);
+  c.m.order = (int32_t*)(b + L.off[Layout::kOrder]);
+  c.m.sorted_slot = (int32_t*)(b + L.off[Layout::kSorted]);
+  c.m.row_of_slot = (int32_t*)(b + L.off[Layout::kRowOf]);
+  c.m.tok_of_row = (int32_t*)(b + L.off[Layout::kTokOf]);
+  c.m.gate_of_row = (float*)(b + L.off[Layout::kGateOf]);
+  c.a = b + L.off[Layout::kA];
+  c.y = b + L.off[Layout::kY];
+  c.u = b + L.off[Layout::kU];
+  c.ag = b + L.off[Layout::kAg];
+  c.dxp = b + L.off[Layout::kDxp];
+  c.dgp = (float*)(b + L.off[Layout::kDgp]);
+  return c;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? MEMFINE_OK : MEMFINE_ERR_HIP; }
+
+GemmArgs gemm_args(const memfine_shape& s, int64_t n, const ChunkBuffers& c) {
+  GemmArgs g = {};
+  g.dtype = s.dtype;
+  g.n = (int)n;
+  g.E = s.E;
+  g.h = s.h;
+  g.F = s.F;
+  g.offsets = c.m.offsets;
+  g.order = c.m.order;
+  g.tok_of_row = c.m.tok_of_row;
+  g.gate_of_row = c.m.gate_of_row;
+  g.a = c.a;
+  g.y = c.y;
+  g.u = c.u;
+  g.ag = c.ag;
+  g.dxp = c.dxp;
+  g.dgp = c.dgp;
+  g.P = dgate_partials(s.F);
+  return g;
+}
+
+// Algorithmic work of one launch, for the timing table.
+struct Work {
+  double flops, bytes;
+};
+Work dispatch_work(int64_t n) { return {0.0, 8.0 * n + 16.0 * n}; }
+
+}  // namespace
+
+// =================================================================== ABI
+extern "C" {
+
+const char* memfine_status_str(int status) {
+  switch (status) {
+    case MEMFINE_OK: return "ok";
+    case MEMFINE_ERR_INVALID_ARG: return "invalid argument";
+    case MEMFINE_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case MEMFINE_ERR_BUDGET: return "memory budget too small for every allowed chunk count";
+    case MEMFINE_ERR_OOM: return "device memory allocation failed";
+    case MEMFINE_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int memfine_plan(const memfine_shape* shape, const int64_t* h_counts, int64_t budget_bytes,
+                 int64_t fixed_bytes, int64_t beta_bytes, const int32_t* bins, int32_t nbins,
+                 int32_t* chunks_out, memfine_plan_info* info) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if (!h_counts || !bins || nbins < 1 || !chunks_out || fixed_bytes < 0 || beta_bytes < 0)
+    return MEMFINE_ERR_INVALID_ARG;
+  int32_t bmin = INT32_MAX, bmax = 0;
+  for (int i = 0; i < nbins; ++i) {
+    if (bins[i] < 1) return MEMFINE_ERR_INVALID_ARG;
+    bmin = std::min(bmin, bins[i]);
+    bmax = std::max(bmax, bins[i]);
+  }
+  __int128 s2 = 0;
+  for (int e = 0; e < shape->E; ++e) {
+    if (h_counts[e] < 0) return MEMFINE_ERR_INVALID_ARG;
+    s2 += h_counts[e];
+  }
+  // Table 2 rows 11-13: D_t (h + 2 g_e + h) bytes per received slot
+  const int64_t beta = beta_bytes > 0 ? beta_bytes : elem_bytes(*shape) * (2 * (int64_t)shape->h + 2 * (int64_t)shape->F);
+  const int64_t avail = budget_bytes - fixed_bytes;
+  int32_t chosen = bmax;
+  int64_t c_theory = -1;
+  bool fits = false;
+  if (avail > 0) {
+    // Eq. (9): c = ceil(s'' / s'_max) = ceil(s'' * beta / avail)
+    const __int128 num = s2 * (__int128)beta;
+    const __int128 c = (num + avail - 1) / avail;
+    c_theory = c > (__int128)INT64_MAX ? INT64_MAX : (int64_t)c;
+    // smallest bin b with b * avail >= s'' * beta
+    int32_t best = INT32_MAX;
+    for (int i = 0; i < nbins; ++i)
+      if ((__int128)bins[i] * avail >= num) best = std::min(best, bins[i]);
+    if (best != INT32_MAX) {
+      chosen = best;
+      fits = true;
+    }
+  }
+  (void)bmin;
+  *chunks_out = chosen;
+  if (info) {
+    info->s_recv = (int64_t)s2;
+    info->beta = beta;
+    info->avail = avail;
+    info->s_max = avail > 0 ? (double)avail / (double)beta : 0.0;
+    info->c_theory = c_theory;
+    info->chunks = chosen;
+    info->fits = fits ? 1 : 0;
+    info->paper_peak_bytes = beta * max_chunk_tokens(shape->T, chosen) * shape->k;
+  }
+  return fits ? MEMFINE_OK : MEMFINE_ERR_BUDGET;
+}
+
+int64_t memfine_workspace_bytes(const memfine_shape* shape, int32_t chunks, int32_t pass) {
+  if (check_shape(shape)) return MEMFINE_ERR_INVALID_ARG;
+  if (chunks < 1 || (pass != MEMFINE_PASS_FWD && pass != MEMFINE_PASS_BWD))
+    return MEMFINE_ERR_INVALID_ARG;
+  const int64_t n = max_chunk_tokens(shape->T, chunks) * shape->k;
+  if (n == 0) return 0;
+  Layout L;
+  chunk_layout(*shape, n, pass, L);
+  return L.total;
+}
+
+int memfine_count(const memfine_shape* shape, const int32_t* d_idx, int32_t* d_work,
+                  int64_t* h_counts, void* stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if (!d_work || !h_counts || (shape->T > 0 && !d_idx)) return MEMFINE_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t nslots = shape->T * shape->k;
+  std::vector<int32_t> host(shape->E + 1, 0);
+  {
+    KernelTimer kt(MEMFINE_K_COUNT, s, 0.0, 4.0 * nslots);
+    if (launch_count(d_idx, nslots, shape->E, d_work, s) != hipSuccess) return MEMFINE_ERR_HIP;
+  }
+  if (hipMemcpyAsync(host.data(), d_work, (shape->E + 1) * sizeof(int32_t), hipMemcpyDeviceToHost,
+                     s) != hipSuccess)
+    return MEMFINE_ERR_HIP;
+  if (hipStreamSynchronize(s) != hipSuccess) return MEMFINE_ERR_HIP;
+  for (int e = 0; e < shape->E; ++e) h_counts[e] = host[e];
+  return host[shape->E] ? MEMFINE_ERR_INVALID_ARG : MEMFINE_OK;
+}
+
+int memfine_dispatch(const memfine_shape* shape, const int32_t* d_idx, int64_t t0, int64_t t1,
+                     int32_t* d_counts, int32_t* d_offsets, int32_t* d_sorted_slot,
+                     int32_t* d_row_of_slot, const memfine_allocator* alloc, void* stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if (t0 < 0 || t1 < t0 || t1 > shape->T) return MEMFINE_ERR_INVALID_ARG;
+  const int64_t n = (t1 - t0) * shape->k;
+  if (!d_counts || !d_offsets || (n > 0 && (!d_idx || !d_sorted_slot || !d_row_of_slot)))
+    return MEMFINE_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t E = shape->E, nb = dispatch_blocks(n);
+  // scratch: bcount, bstart, order, tok_of_row, gate_of_row
+  const int64_t o_bstart = align256(E * nb * 4), o_order = o_bstart + align256(E * nb * 4);
+  const int64_t o_tok = o_order + align256(E * 4), o_gate = o_tok + align256(n * 4);
+  const int64_t total = o_gate + align256(n * 4);
+  char* scratch = (char*)ws_alloc(alloc, (size_t)total, s);
+  if (!scratch) return MEMFINE_ERR_OOM;
+  ChunkMeta m;
+  m.bcount = (int32_t*)scratch;
+  m.bstart = (int32_t*)(scratch + o_bstart);
+  m.order = (int32_t*)(scratch + o_order);
+  m.tok_of_row = (int32_t*)(scratch + o_tok);
+  m.gate_of_row = (float*)(scratch + o_gate);
+  m.counts = d_counts;
+  m.offsets = d_offsets;
+  m.sorted_slot = d_sorted_slot;
+  m.row_of_slot = d_row_of_slot;
+  hipError_t err;
+  {
+    KernelTimer kt(MEMFINE_K_DISPATCH, s, 0.0, dispatch_work(n).bytes);
+    err = launch_dispatch(d_idx, nullptr, t0 * shape->k, (int)n, shape->E, shape->k, m, s);
+  }
+  ws_release(alloc, scratch, (size_t)total, s);
+  return hip_status(err);
+}
+
+int memfine_moe_fwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
+                    const int32_t* d_idx, const float* d_gates, const void* d_W1,
+                    const void* d_W2, void* d_Y, const memfine_allocator* alloc, void* stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if (chunks < 1) return MEMFINE_ERR_INVALID_ARG;
+  const memfine_shape& S = *shape;
+  if (S.T == 0) return MEMFINE_OK;
+  if (!d_X || !d_idx || !d_gates || !d_W1 || !d_W2 || !d_Y) return MEMFINE_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t C = std::min<int64_t>(chunks, S.T);
+  const double es = (double)elem_bytes(S);
+  for (int64_t i = 0; i < C; ++i) {
+    const int64_t t0 = i * S.T / C, t1 = (i + 1) * S.T / C;
+    const int64_t tokens = t1 - t0, n = tokens * S.k;
+    if (n == 0) continue;
+    Layout L;
+    chunk_layout(S, n, MEMFINE_PASS_FWD, L);
+    void* ws = ws_alloc(alloc, (size_t)L.total, s);
+    if (!ws) return MEMFINE_ERR_OOM;
+    const ChunkBuffers cb = carve(ws, L);
+    GemmArgs g = gemm_args(S, n, cb);
+    g.X = d_X;
+    g.W1 = d_W1;
+    g.W2 = d_W2;
+    hipError_t err;
+    {
+      KernelTimer kt(MEMFINE_K_DISPATCH, s, 0.0, dispatch_work(n).bytes);
+      err = launch_dispatch(d_idx, d_gates, t0 * S.k, (int)n, S.E, S.k, cb.m, s);
+    }
+    const double hF = (double)S.h * S.F, nd = (double)n, Ed = S.E;
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC1, s, 4.0 * nd * hF,
+                     es * (tokens * (double)S.h + 2.0 * Ed * hF + nd * S.F));
+      err = launch_fc1_fwd(g, s);
+    }
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC2, s, 2.0 * nd * hF, es * (nd * S.F + Ed * hF + nd * S.h));
+      err = launch_fc2_fwd(g, s);
+    }
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_COMBINE, s, 2.0 * nd * S.h,
+                     es * (nd * S.h + tokens * (double)S.h) + 8.0 * nd);
+      err = launch_combine(S.dtype, cb.y, cb.m.row_of_slot, d_gates, t0, (int)tokens, S.h, S.k,
+                           d_Y, s);
+    }
+    ws_release(alloc, ws, (size_t)L.total, s);
+    if (err != hipSuccess) return MEMFINE_ERR_HIP;
+  }
+  return MEMFINE_OK;
+}
+
+int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
+                    const int32_t* d_idx, const float* d_gates, const void* d_W1,
+                    const void* d_W2, const void* d_dY, void* d_dX, float* d_dW1, float* d_dW2,
+                    float* d_dgates, int32_t accumulate_dW, const memfine_allocator* alloc,
+                    void* stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if (chunks < 1 || (accumulate_dW != 0 && accumulate_dW != 1)) return MEMFINE_ERR_INVALID_ARG;
+  const memfine_shape& S = *shape;
+  if (!d_W1 || !d_W2 || !d_dW1 || !d_dW2) return MEMFINE_ERR_INVALID_ARG;
+  if (S.T > 0 && (!d_X || !d_idx || !d_gates || !d_dY || !d_dX || !d_dgates))
+    return MEMFINE_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  const double es = (double)elem_bytes(S);
+  const double hF = (double)S.h * S.F, Ed = S.E;
+  if (S.T == 0) {
+    if (accumulate_dW) return MEMFINE_OK;
+    // no rows at all: the weight gradients are zero
+    const int64_t w1 = (int64_t)S.E * 2 * S.F * S.h, w2 = (int64_t)S.E * S.h * S.F;
+    hipError_t err = launch_fill_i32((int32_t*)d_dW1, w1, 0, s);
+    if (err == hipSuccess) err = launch_fill_i32((int32_t*)d_dW2, w2, 0, s);
+    return hip_status(err);
+  }
+  const int64_t C = std::min<int64_t>(chunks, S.T);
+  bool first = true;
+  for (int64_t i = 0; i < C; ++i) {
+    const int64_t t0 = i * S.T / C, t1 = (i + 1) * S.T / C;
+    const int64_t tokens = t1 - t0, n = tokens * S.k;
+    if (n == 0) continue;
+    Layout L;
+    chunk_layout(S, n, MEMFINE_PASS_BWD, L);
+    void* ws = ws_alloc(alloc, (size_t)L.total, s);
+    if (!ws) return MEMFINE_ERR_OOM;
+    const ChunkBuffers cb = carve(ws, L);
+    GemmArgs g = gemm_args(S, n, cb);
+    g.X = d_X;
+    g.dY = d_dY;
+    g.W1 = d_W1;
+    g.W2 = d_W2;
+    g.dW1 = d_dW1;
+    g.dW2 = d_dW2;
+    g.accumulate = (accumulate_dW || !first) ? 1 : 0;
+    const double nd = (double)n, td = (double)tokens;
+    const double dw_rmw = g.accumulate ? 8.0 : 4.0;
+    hipError_t err;
+    {
+      KernelTimer kt(MEMFINE_K_DISPATCH, s, 0.0, dispatch_work(n).bytes);
+      err = launch_dispatch(d_idx, d_gates, t0 * S.k, (int)n, S.E, S.k, cb.m, s);
+    }
+    if (err == hipSuccess) {  // recompute F_w(X_i): u and g * a
+      KernelTimer kt(MEMFINE_K_FC1_RECOMP, s, 4.0 * nd * hF,
+                     es * (td * S.h + 2.0 * Ed * hF + 3.0 * nd * S.F));
+      err = launch_fc1_recompute(g, s);
+    }
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC2_DGRAD, s, 2.0 * nd * hF,
+                     es * (td * S.h + Ed * hF + 4.0 * nd * S.F) + 4.0 * nd * g.P);
+      err = launch_fc2_dgrad(g, s);
+    }
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC2_WGRAD, s, 2.0 * nd * hF,
+                     es * (td * S.h + nd * S.F) + dw_rmw * Ed * hF);
+      err = launch_fc2_wgrad(g, s);
+    }
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC1_WGRAD, s, 4.0 * nd * hF,
+                     es * (2.0 * nd * S.F + td * S.h) + 2.0 * dw_rmw * Ed * hF);
+      err = launch_fc1_wgrad(g, s);
+    }
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC1_DGRAD, s, 4.0 * nd * hF,
+                     es * (2.0 * nd * S.F + 2.0 * Ed * hF + nd * S.h));
+      err = launch_fc1_dgrad(g, s);
+    }
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_UNPERMUTE, s, nd * S.h,
+                     es * (nd * S.h + td * S.h) + 4.0 * nd * (g.P + 2));
+      err = launch_unpermute(S.dtype, cb.dxp, cb.dgp, g.P, cb.m.row_of_slot, t0, (int)tokens,
+                             S.h, S.k, d_dX, d_dgates, s);
+    }
+    ws_release(alloc, ws, (size_t)L.total, s);
+    if (err != hipSuccess) return MEMFINE_ERR_HIP;
+    first = false;
+  }
+  return MEMFINE_OK;
+}
+
+int memfine_profile_begin(uint32_t mask) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (auto& r : g_prof) {
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+  }
+  g_prof.clear();
+  g_prof_mask = mask;
+  return MEMFINE_OK;
+}
+
+int memfine_profile_end(memfine_kernel_stat* out) {
+  if (!out) return MEMFINE_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_mask = 0;
+  for (int i = 0; i < MEMFINE_K_NUM; ++i) out[i] = memfine_kernel_stat{0, 0.0, 0.0, 0.0};
+  int rc = MEMFINE_OK;
+  for (auto& r : g_prof) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.stop) != hipSuccess ||
+        hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess)
+      rc = MEMFINE_ERR_HIP;
+    memfine_kernel_stat& st = out[r.id];
+    st.launches += 1;
+    st.total_ms += ms;
+    st.flops += r.flops;
+    st.bytes += r.bytes;
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+  }
+  g_prof.clear();
+  return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,121 @@
+// Memory-bound gather/sum kernels of the chunked MoE layer.
+//
+// combine:    the gate-weighted sum over a token's k slots that follows the
+//             expert (Table 2 "score mul" and "add"; the "combine" of
+//             Eq. (4)): Y[t] = sum_j g[t,j] * y[row(t,j)], j ascending, fp32.
+// unpermute:  its backward for the input gradient, dX[t] = sum_j dxp[row(t,j)]
+//             (the concatenation of Eq. (7) fills dX chunk by chunk), and the
+//             gate gradient dg[t,j] = sum of the per-tile partial dot products
+//             the FC2 backward kernel leaves for row(t,j).
+// Each thread moves one 16-byte vector of a row; consecutive threads take
+// consecutive vectors, so every row is read and written with full coalescing.
+#include "common.h"
+#include "kernels.h"
+
+namespace memfine {
+
+template <typename T>
+__global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
+                                                      const int32_t* __restrict__ row_of_slot,
+                                                      const float* __restrict__ gates, int64_t t0,
+                                                      int tokens, int h, int k,
+                                                      T* __restrict__ Y) {
+  constexpr int V = Elem<T>::kVec;
+  const int vpr = h / V;
+  const int64_t gid = blockIdx.x * 256ll + threadIdx.x;
+  if (gid >= (int64_t)tokens * vpr) return;
+  const int i = (int)(gid / vpr), c = (int)(gid % vpr);
+  const int64_t t = t0 + i;
+  float acc[V];
+#pragma unroll
+  for (int q = 0; q < V; ++q) acc[q] = 0.f;
+  for (int j = 0; j < k; ++j) {
+    const int r = row_of_slot[(int64_t)i * k + j];
+    if (r < 0) continue;  // dropped slot
+    const float g = gates[t * k + j];
+    const u32x4_t v = *(const u32x4_t*)(y + (int64_t)r * h + c * V);
+    float f[V];
+    unpack16(v, f, (T*)nullptr);
+#pragma unroll
+    for (int q = 0; q < V; ++q) acc[q] = fmaf(g, f[q], acc[q]);
+  }
+  *(u32x4_t*)(Y + t * h + c * V) = pack16(acc, (T*)nullptr);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void unpermute_kernel(const T* __restrict__ dxp,
+                                                        const int32_t* __restrict__ row_of_slot,
+                                                        int64_t t0, int tokens, int h, int k,
+                                                        T* __restrict__ dX) {
+  constexpr int V = Elem<T>::kVec;
+  const int vpr = h / V;
+  const int64_t gid = blockIdx.x * 256ll + threadIdx.x;
+  if (gid >= (int64_t)tokens * vpr) return;
+  const int i = (int)(gid / vpr), c = (int)(gid % vpr);
+  float acc[V];
+#pragma unroll
+  for (int q = 0; q < V; ++q) acc[q] = 0.f;
+  for (int j = 0; j < k; ++j) {
+    const int r = row_of_slot[(int64_t)i * k + j];
+    if (r < 0) continue;  // dropped slot
+    const u32x4_t v = *(const u32x4_t*)(dxp + (int64_t)r * h + c * V);
+    float f[V];
+    unpack16(v, f, (T*)nullptr);
+#pragma unroll
+    for (int q = 0; q < V; ++q) acc[q] += f[q];
+  }
+  *(u32x4_t*)(dX + (t0 + i) * h + c * V) = pack16(acc, (T*)nullptr);
+}
+
+// One thread per slot of the chunk: dgates[slot] = sum over p of dgp[row][p].
+__global__ __launch_bounds__(256) void dgate_kernel(const float* __restrict__ dgp, int P,
+                                                    const int32_t* __restrict__ row_of_slot,
+                                                    int64_t slot0, int nslots,
+                                                    float* __restrict__ dgates) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= nslots) return;
+  const int r = row_of_slot[i];
+  float s = 0.f;
+  if (r >= 0) {
+    const float* p = dgp + (int64_t)r * P;
+    for (int q = 0; q < P; ++q) s += p[q];
+  }
+  dgates[slot0 + i] = s;
+}
+
+hipError_t launch_combine(int dtype, const void* y, const int32_t* row_of_slot, const float* gates,
+                          int64_t t0, int tokens, int h, int k, void* Y, hipStream_t s) {
+  const int V = dtype == 0 ? 8 : 4;
+  const int64_t work = (int64_t)tokens * (h / V);
+  if (work == 0) return hipSuccess;
+  const int blocks = (int)((work + 255) / 256);
+  if (dtype == 0)
+    combine_kernel<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t*)y, row_of_slot, gates, t0, tokens,
+                                                  h, k, (bf16_t*)Y);
+  else
+    combine_kernel<float><<<blocks, 256, 0, s>>>((const float*)y, row_of_slot, gates, t0, tokens, h,
+                                                 k, (float*)Y);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpermute(int dtype, const void* dxp, const float* dgp, int P,
+                            const int32_t* row_of_slot, int64_t t0, int tokens, int h, int k,
+                            void* dX, float* dgates, hipStream_t s) {
+  const int V = dtype == 0 ? 8 : 4;
+  const int64_t work = (int64_t)tokens * (h / V);
+  if (work == 0) return hipSuccess;
+  const int blocks = (int)((work + 255) / 256);
+  if (dtype == 0)
+    unpermute_kernel<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t*)dxp, row_of_slot, t0, tokens, h,
+                                                    k, (bf16_t*)dX);
+  else
+    unpermute_kernel<float><<<blocks, 256, 0, s>>>((const float*)dxp, row_of_slot, t0, tokens, h, k,
+                                                   (float*)dX);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const int nslots = tokens * k;
+  dgate_kernel<<<(nslots + 255) / 256, 256, 0, s>>>(dgp, P, row_of_slot, t0 * k, nslots, dgates);
+  return hipGetLastError();
+}
+
+}  // namespace memfine

@@ -1,0 +1,78 @@
+// Host-side launchers of the gfx950 kernels (internal to libmemfine).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace memfine {
+
+// Slots handled by one workgroup of the dispatch histogram / scatter kernels.
+constexpr int kDispatchSlotsPerBlock = 2048;
+
+inline int dispatch_blocks(int64_t n) {
+  return (int)((n + kDispatchSlotsPerBlock - 1) / kDispatchSlotsPerBlock);
+}
+
+// Per-chunk routing metadata produced by the dispatch kernels; all device.
+struct ChunkMeta {
+  int32_t* bcount;       // [E * nb]  per-workgroup expert histograms (expert-major)
+  int32_t* bstart;       // [E * nb]  their exclusive scan = first output row
+  int32_t* counts;       // [E]
+  int32_t* offsets;      // [E + 1]
+  int32_t* order;        // [E]       experts by descending count (ties: lower id)
+  int32_t* sorted_slot;  // [n]       global slot id of each grouped row
+  int32_t* row_of_slot;  // [n]       grouped row of the chunk's i-th slot
+  int32_t* tok_of_row;   // [n]       token of each grouped row
+  float* gate_of_row;    // [n]       gate of each grouped row
+};
+
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
+hipError_t launch_count(const int32_t* idx, int64_t nslots, int E, int32_t* work, hipStream_t s);
+// Dispatch of slots [slot0, slot0 + n) of the flat idx array (one chunk).
+hipError_t launch_dispatch(const int32_t* idx, const float* gates, int64_t slot0, int n, int E,
+                           int k, const ChunkMeta& m, hipStream_t s);
+
+// Gate-weighted combine, Y[t0 + i] = sum_j g[t, j] * y[row_of_slot[i*k + j]].
+hipError_t launch_combine(int dtype, const void* y, const int32_t* row_of_slot, const float* gates,
+                          int64_t t0, int tokens, int h, int k, void* Y, hipStream_t s);
+// dX[t0 + i] = sum_j dxp[row_of_slot[i*k + j]];  dgates[t, j] = sum_p dgp[row][p].
+hipError_t launch_unpermute(int dtype, const void* dxp, const float* dgp, int P,
+                            const int32_t* row_of_slot, int64_t t0, int tokens, int h, int k,
+                            void* dX, float* dgates, hipStream_t s);
+
+// Grouped GEMMs.  Row-grouped problems: rows [offsets[e], offsets[e+1]) belong
+// to expert e.  n is the chunk's slot count (an upper bound for the grid).
+struct GemmArgs {
+  int dtype;
+  int n, E, h, F;
+  const int32_t* offsets;
+  const int32_t* order;
+  const int32_t* tok_of_row;
+  const float* gate_of_row;
+  const void* X;     // [T, h]
+  const void* dY;    // [T, h]
+  const void* W1;    // [E, 2F, h]
+  const void* W2;    // [E, h, F]
+  void* a;           // [n, F]   forward SwiGLU output
+  void* y;           // [n, h]   forward expert output
+  void* u;           // [n, 2F]  backward: FC1 recompute output, then du in place
+  void* ag;          // [n, F]   backward: gate * SwiGLU output
+  void* dxp;         // [n, h]   backward: input gradient per row
+  float* dgp;        // [n, P]   backward: partial gate gradients
+  int P;             // partials per row
+  float* dW1;        // [E, 2F, h]
+  float* dW2;        // [E, h, F]
+  int accumulate;    // wgrad: 1 = add into dW, 0 = overwrite
+};
+
+int dgate_partials(int F);
+
+hipError_t launch_fc1_fwd(const GemmArgs& g, hipStream_t s);
+hipError_t launch_fc2_fwd(const GemmArgs& g, hipStream_t s);
+hipError_t launch_fc1_recompute(const GemmArgs& g, hipStream_t s);
+hipError_t launch_fc2_dgrad(const GemmArgs& g, hipStream_t s);
+hipError_t launch_fc2_wgrad(const GemmArgs& g, hipStream_t s);
+hipError_t launch_fc1_wgrad(const GemmArgs& g, hipStream_t s);
+hipError_t launch_fc1_dgrad(const GemmArgs& g, hipStream_t s);
+
+}  // namespace memfine

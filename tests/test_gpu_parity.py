@@ -1,0 +1,311 @@
+"""GPU parity: the HIP layer, called through the C ABI, against the fp64
+oracle on the same seeded inputs.
+
+* counts and the dispatch permutation: bit-exact;
+* outputs and gradients: max|got - ref| / max|ref| <= 2e-2 (bf16 inputs,
+  fp32 accumulation) and <= 1e-4 (fp32 path), per tensor;
+* Y, dX and dgates bit-identical for every chunk count (each row's dot
+  products do not depend on how rows are grouped into tiles or chunks), and
+  the whole layer bitwise deterministic run to run;
+* full-size workloads in the launch configuration the benchmark times, on
+  sampled tokens and sampled weight-gradient columns the oracle computes one
+  by one.
+"""
+import numpy as np
+import pytest
+
+import moe_workloads as mw
+from gpu_harness import (TOL, device_case, host, log, relerr, run_bwd, run_fwd, shape_of,
+                         torch)
+from oracle import moe as om
+
+pytestmark = pytest.mark.gpu
+
+W = mw.WORKLOADS
+SMALL = {
+    "cfg1-f32": W[1],
+    "cfg2-like": mw.scaled(W[2], T=768, h=256, F=192),
+    "cfg3-like": mw.scaled(W[3], T=1024, h=384, F=448),
+    "cfg4-like": mw.scaled(W[4], T=256, h=448, F=128),
+    "cfg5-like": mw.scaled(W[5], T=512, h=128, F=192),
+}
+
+
+@pytest.fixture(scope="module")
+def mf():
+    t = torch()
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2511_21431_amd as m
+    m.lib()
+    return m
+
+
+_cache = {}
+
+
+def small_case(name, seed=None):
+    key = (name, seed)
+    if key not in _cache:
+        w = SMALL[name]
+        s = seed if seed is not None else 101 + list(SMALL).index(name)
+        _cache[key] = (w, mw.make_case(w, s))
+    return _cache[key]
+
+
+# ------------------------------------------------------------------ dispatch
+@pytest.mark.parametrize("name", list(SMALL))
+def test_count_matches_oracle(mf, name):
+    w, case = small_case(name)
+    t = torch()
+    log(f"count {name}")
+    idx = t.from_numpy(case["idx"]).cuda()
+    work = t.zeros(w.E + 1, dtype=t.int32, device="cuda")
+    got = mf.memfine_count(shape_of(w), idx, work)
+    assert got.tolist() == om.expert_counts(case["idx"], w.E).tolist()
+
+
+def test_count_rejects_bad_ids(mf):
+    t = torch()
+    w = SMALL["cfg2-like"]
+    idx = t.zeros((w.T, w.k), dtype=t.int32, device="cuda")
+    idx[5, 1] = w.E
+    idx[7, 0] = -3
+    work = t.zeros(w.E + 1, dtype=t.int32, device="cuda")
+    with pytest.raises(mf.MemfineError) as ei:
+        mf.memfine_count(shape_of(w), idx, work)
+    assert ei.value.code == -1
+    assert int(work[w.E]) == 2
+
+
+def _dispatch_check(mf, w, idx_np, t0, t1):
+    t = torch()
+    n = (t1 - t0) * w.k
+    idx = t.from_numpy(np.ascontiguousarray(idx_np, dtype=np.int32)).cuda()
+    counts = t.full((w.E,), -7, dtype=t.int32, device="cuda")
+    offsets = t.full((w.E + 1,), -7, dtype=t.int32, device="cuda")
+    ss = t.full((n,), -7, dtype=t.int32, device="cuda")
+    rs = t.full((n,), -7, dtype=t.int32, device="cuda")
+    mf.memfine_dispatch(shape_of(w), idx, t0, t1, counts, offsets, ss, rs)
+    ref = om.dispatch(idx_np, t0, t1, w.E)
+    assert counts.cpu().numpy().tolist() == ref["counts"].tolist()
+    assert offsets.cpu().numpy().tolist() == ref["offsets"].tolist()
+    assert ss.cpu().numpy().tolist() == ref["sorted_slot"].tolist()
+    assert rs.cpu().numpy().tolist() == ref["row_of_slot"].tolist()
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_dispatch_bit_exact_every_chunk(mf, name):
+    w, case = small_case(name)
+    for C in (1, 2, 3, 4, 8):
+        for t0, t1 in om.chunk_ranges(w.T, C):
+            log(f"dispatch {name} C={C} [{t0},{t1})")
+            _dispatch_check(mf, w, case["idx"], t0, t1)
+
+
+@pytest.mark.parametrize("E,k,T", [(1, 1, 1), (1, 3, 5000), (1024, 8, 3000), (1000, 1, 777),
+                                   (7, 2, 0), (64, 6, 4096)])
+def test_dispatch_edge_shapes(mf, E, k, T):
+    w = mw.Workload("edge", T=T, h=64, F=64, E=E, k=k, dtype="bf16", routing="dirichlet")
+    rng = np.random.default_rng(E * 7 + k)
+    idx = rng.integers(0, E, size=(T, k)).astype(np.int32)
+    if E > 4 and T > 0:
+        idx[: T // 2] = E - 1            # a hot expert and long runs of equal ids
+    log(f"dispatch edge E={E} k={k} T={T}")
+    _dispatch_check(mf, w, idx, 0, T)
+    if T > 3:
+        _dispatch_check(mf, w, idx, 1, T - 2)
+
+
+def test_dispatch_full_size_config4(mf):
+    w = W[4]
+    idx, _ = mw.make_routing(w, 4)
+    for C in (1, 4, 8):
+        for t0, t1 in om.chunk_ranges(w.T, C)[:2]:
+            log(f"dispatch cfg4 C={C} [{t0},{t1})")
+            _dispatch_check(mf, w, idx, t0, t1)
+
+
+# ------------------------------------------------------------- layer parity
+CHUNKS = {"cfg1-f32": (1, 2, 4), "cfg2-like": (1, 2, 4), "cfg3-like": (1, 3, 8),
+          "cfg4-like": (1, 4), "cfg5-like": (1, 16)}
+
+
+@pytest.mark.parametrize("name,C", [(n, c) for n in SMALL for c in CHUNKS[n]])
+def test_layer_parity(mf, name, C):
+    w, case = small_case(name)
+    tol = TOL[w.dtype]
+    dev = device_case(w, case)
+    log(f"fwd {name} C={C}")
+    Y = run_fwd(w, dev, C)
+    log(f"bwd {name} C={C}")
+    B = run_bwd(w, dev, C)
+    torch().cuda.synchronize()
+    Y_ref = om.moe_fwd(case["X"], case["idx"], case["gates"], case["W1"], case["W2"], C)
+    R = om.moe_bwd(case["X"], case["idx"], case["gates"], case["W1"], case["W2"], case["dY"], C)
+    errs = {"Y": relerr(host(Y), Y_ref)}
+    for key in ("dX", "dgates", "dW1", "dW2"):
+        errs[key] = relerr(host(B[key]), R[key])
+    log(f"  {name} C={C} rel errors: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    for key, e in errs.items():
+        assert e <= tol, (key, e)
+
+
+@pytest.mark.parametrize("name", ["cfg1-f32", "cfg3-like", "cfg4-like"])
+def test_chunk_invariance_and_determinism(mf, name):
+    w, case = small_case(name)
+    dev = device_case(w, case)
+    ref_Y = host(run_fwd(w, dev, 1))
+    ref_B = {k: host(v) for k, v in run_bwd(w, dev, 1).items()}
+    for C in (1, 2, 5, w.T, w.T + 3):
+        log(f"invariance {name} C={C}")
+        Y = host(run_fwd(w, dev, C))
+        B = {k: host(v) for k, v in run_bwd(w, dev, C).items()}
+        assert np.array_equal(Y, ref_Y), C
+        assert np.array_equal(B["dX"], ref_B["dX"]), C
+        assert np.array_equal(B["dgates"], ref_B["dgates"]), C
+        for key in ("dW1", "dW2"):
+            if C == 1:
+                assert np.array_equal(B[key], ref_B[key])      # run-to-run determinism
+            else:
+                assert relerr(B[key], ref_B[key]) < 1e-5, (C, key)
+
+
+def test_accumulate_dW(mf):
+    w, case = small_case("cfg2-like")
+    t = torch()
+    dev = device_case(w, case)
+    base1 = t.randn((w.E, 2 * w.F, w.h), device="cuda")
+    base2 = t.randn((w.E, w.h, w.F), device="cuda")
+    dW = (base1.clone(), base2.clone())
+    log("accumulate dW")
+    run_bwd(w, dev, 3, dW=dW, accumulate=True)
+    plain = run_bwd(w, dev, 3)
+    assert relerr(host(dW[0] - base1), host(plain["dW1"])) < 1e-5
+    assert relerr(host(dW[1] - base2), host(plain["dW2"])) < 1e-5
+
+
+def test_degenerate_cases(mf):
+    t = torch()
+    # one token, one slot, one expert
+    w = mw.Workload("one", T=1, h=64, F=64, E=1, k=1, dtype="f32", routing="dirichlet")
+    case = mw.make_case(w, 3)
+    dev = device_case(w, case)
+    log("degenerate T=1")
+    Y = host(run_fwd(w, dev, 4))
+    B = run_bwd(w, dev, 4)
+    assert relerr(Y, om.moe_fwd(case["X"], case["idx"], case["gates"], case["W1"], case["W2"])) < 1e-4
+    R = om.moe_bwd(case["X"], case["idx"], case["gates"], case["W1"], case["W2"], case["dY"])
+    for key in ("dX", "dgates", "dW1", "dW2"):
+        assert relerr(host(B[key]), R[key]) < 1e-4
+    # experts that receive nothing get zero weight gradients
+    w = mw.Workload("cold", T=64, h=128, F=64, E=6, k=2, dtype="bf16", routing="dirichlet")
+    case = mw.make_case(w, 4)
+    case["idx"][:] = np.where(case["idx"] % 2 == 0, 0, 3).astype(np.int32)
+    dev = device_case(w, case)
+    log("degenerate cold experts")
+    B = run_bwd(w, dev, 2)
+    dW1 = host(B["dW1"])
+    for e in (1, 2, 4, 5):
+        assert np.all(dW1[e] == 0.0)
+    # no tokens at all
+    w0 = mw.Workload("empty", T=0, h=64, F=64, E=3, k=2, dtype="bf16", routing="dirichlet")
+    import paper_2511_21431_amd as m
+    X = t.zeros((0, 64), dtype=t.bfloat16, device="cuda")
+    idx = t.zeros((0, 2), dtype=t.int32, device="cuda")
+    g = t.zeros((0, 2), dtype=t.float32, device="cuda")
+    W1 = t.ones((3, 128, 64), dtype=t.bfloat16, device="cuda")
+    W2 = t.ones((3, 64, 64), dtype=t.bfloat16, device="cuda")
+    dW1 = t.full((3, 128, 64), 5.0, device="cuda")
+    dW2 = t.full((3, 64, 64), 5.0, device="cuda")
+    m.memfine_moe_fwd(shape_of(w0), 2, X, idx, g, W1, W2, X)
+    m.memfine_moe_bwd(shape_of(w0), 2, X, idx, g, W1, W2, X, X, dW1, dW2, g)
+    assert float(dW1.abs().max()) == 0.0 and float(dW2.abs().max()) == 0.0
+
+
+def test_allocator_hook_peak_and_oom(mf):
+    """The working memory the layer holds at once, measured two ways (the
+    allocator hook's own high-water mark, and torch's allocator statistics),
+    against the layer's declared per-chunk workspace."""
+    t = torch()
+    w, case = small_case("cfg4-like")
+    dev = device_case(w, case)
+    s = shape_of(w)
+    dt = t.bfloat16
+    dX = t.empty((w.T, w.h), dtype=dt, device="cuda")
+    dg = t.empty((w.T, w.k), device="cuda")
+    dW1 = t.empty((w.E, 2 * w.F, w.h), device="cuda")
+    dW2 = t.empty((w.E, w.h, w.F), device="cuda")
+    for C in (1, 2, 4):
+        alloc = mf.TorchAllocator()
+        t.cuda.synchronize()
+        t.cuda.empty_cache()
+        t.cuda.reset_peak_memory_stats()
+        base = t.cuda.memory_allocated()
+        log(f"allocator peak C={C}")
+        mf.memfine_moe_bwd(s, C, dev["X"], dev["idx"], dev["gates"], dev["W1"], dev["W2"],
+                           dev["dY"], dX, dW1, dW2, dg, allocator=alloc)
+        t.cuda.synchronize()
+        peak = t.cuda.max_memory_allocated() - base
+        pred = mf.memfine_workspace_bytes(s, C, mf.PASS_BWD)
+        assert alloc.live == {} and alloc.live_bytes == 0
+        assert alloc.high_water == pred, (C, alloc.high_water, pred)
+        # torch rounds blocks up (at most to the next 2 MiB segment)
+        assert pred <= peak <= pred + (2 << 20), (C, peak, pred)
+    alloc = mf.TorchAllocator()
+    alloc.fail_at = 2                       # second chunk's allocation fails
+    with pytest.raises(mf.MemfineError) as ei:
+        run_bwd(w, dev, 3, allocator=alloc)
+    assert ei.value.code == -4 and alloc.live == {}
+
+
+# ---------------------------------------------------- full-size, sampled
+FULL = [(2, 2), (2, 1), (3, 4), (4, 4)]
+
+
+@pytest.mark.parametrize("cfg,C", FULL)
+def test_full_size_sampled(mf, cfg, C):
+    t = torch()
+    w = W[cfg]
+    log(f"full-size cfg{cfg} C={C}: generating inputs")
+    idx, gates = mw.make_routing(w, cfg)
+    dev = mw.make_tensors_device(w, cfg, "cuda")
+    dev["idx"] = t.from_numpy(idx).cuda()
+    dev["gates"] = t.from_numpy(gates).cuda()
+    log(f"full-size cfg{cfg} C={C}: fwd")
+    Y = run_fwd(w, dev, C)
+    log(f"full-size cfg{cfg} C={C}: bwd")
+    B = run_bwd(w, dev, C)
+    t.cuda.synchronize()
+    rng = np.random.default_rng(1000 + cfg)
+    toks = sorted(set(rng.choice(w.T, size=12, replace=False).tolist()) | {0, w.T - 1})
+    X = dev["X"].float().cpu().numpy()
+    dY = dev["dY"].float().cpu().numpy()
+    counts = np.bincount(idx.reshape(-1), minlength=w.E)
+    order = np.argsort(-counts, kind="stable")
+    experts = sorted({int(order[0]), int(order[w.E // 2]), int(order[-1])} |
+                     {int(e) for e in np.unique(idx[toks])})
+    W1 = {e: dev["W1"][e].double().cpu().numpy() for e in experts}
+    W2 = {e: dev["W2"][e].double().cpu().numpy() for e in experts}
+
+    class Lazy(dict):           # W1[e] lookups for the token forms
+        def __getitem__(self, e):
+            return dict.__getitem__(self, int(e))
+
+    W1l, W2l = Lazy(W1), Lazy(W2)
+    W1l.shape = (w.E, 2 * w.F, w.h)
+    log(f"full-size cfg{cfg} C={C}: oracle on {len(toks)} tokens")
+    Y_ref = om.moe_fwd_tokens(X, idx, gates, W1l, W2l, toks)
+    dX_ref, dg_ref = om.moe_bwd_tokens(X, idx, gates, W1l, W2l, dY, toks)
+    tol = TOL[w.dtype]
+    errs = {"Y": relerr(host(Y[toks]), Y_ref), "dX": relerr(host(B["dX"][toks]), dX_ref),
+            "dgates": relerr(host(B["dgates"][toks]), dg_ref)}
+    fs = sorted(set(rng.choice(w.F, size=3, replace=False).tolist()) | {0, w.F - 1})
+    for e in (int(order[0]), int(order[w.E // 2]), int(order[-1])):
+        g1, u1, c2 = om.moe_dW_expert_columns(X, idx, gates, W1l, W2l, dY, e, fs)
+        errs[f"dW1g[{e}]"] = relerr(host(B["dW1"][e][fs]), g1)
+        errs[f"dW1u[{e}]"] = relerr(host(B["dW1"][e][[w.F + f for f in fs]]), u1)
+        errs[f"dW2[{e}]"] = relerr(host(B["dW2"][e][:, fs]), c2)
+    log(f"  cfg{cfg} C={C}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    for key, e in errs.items():
+        assert e <= tol, (key, e)

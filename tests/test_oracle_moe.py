@@ -238,3 +238,14 @@ def test_planted_mistakes_are_caught(monkeypatch, mistake):
         monkeypatch.setattr(om, "chunk_ranges",
                             lambda T, C: [(max(0, i * T // C - 1), (i + 1) * T // C) for i in range(C)])
     assert _autograd_gap() > 1e-6 or fd_error() > 1e-6
+
+
+def test_dW_columns_match_full():
+    X, idx, g, W1, W2, dY = tiny_case(T=12, h=8, F=8, E=4, k=3, seed=9)
+    B = om.moe_bwd(X, idx, g, W1, W2, dY, 2)
+    fs = [0, 3, 7]
+    for e in range(4):
+        g1, u1, c2 = om.moe_dW_expert_columns(X, idx, g, W1, W2, dY, e, fs)
+        assert rel(g1, B["dW1"][e][fs]) < 1e-12
+        assert rel(u1, B["dW1"][e][[8 + f for f in fs]]) < 1e-12
+        assert rel(c2, B["dW2"][e][:, fs]) < 1e-12
