@@ -3,6 +3,7 @@
 // allocates, fills and releases every chunk's buffers in stream order
 // (paper Section 4.1, Eq. (6)/(7); Section 4.2, Eq. (8)/(9)).
 #include <algorithm>
+#include <cstdlib>
 #include <mutex>
 #include <unordered_map>
 #include <vector>
@@ -57,6 +58,11 @@ int check_shape(const memfine_shape* s) {
     return MEMFINE_ERR_INVALID_ARG;
   if (s->dtype != MEMFINE_BF16 && s->dtype != MEMFINE_F32) return MEMFINE_ERR_UNSUPPORTED;
   if (s->T * (int64_t)s->k >= (int64_t(1) << 31)) return MEMFINE_ERR_UNSUPPORTED;
+  // the kernels address X, dY and one expert's weights with 31-bit offsets
+  const int64_t es = s->dtype == MEMFINE_BF16 ? 2 : 4;
+  if (s->T * (int64_t)s->h * es >= (int64_t(1) << 31) ||
+      (int64_t)2 * s->F * (int64_t)s->h * es >= (int64_t(1) << 31))
+    return MEMFINE_ERR_UNSUPPORTED;
   return MEMFINE_OK;
 }
 
@@ -187,6 +193,29 @@ ChunkBuffers carve(void* base, const Layout& L) {
   return c;
 }
 
+// MEMFINE_TILE pins the bf16 GEMM tile shape for measurements (1..7, see
+// launch_auto in grouped_gemm.hip; 128 = 1, 256 = 2).
+int tile_override() {
+  static const int v = [] {
+    const char* e = getenv("MEMFINE_TILE");
+    if (!e) return 0;
+    const int t = atoi(e);
+    return t == 128 ? 1 : t == 256 ? 2 : (t >= 1 && t <= 7) ? t : 0;
+  }();
+  return v;
+}
+
+// MEMFINE_RASTER selects the GEMM tile traversal (0..3; default 0: row-major,
+// which measured at least as fast as the XCD-grouped orders).
+int raster_mode() {
+  static const int v = [] {
+    const char* e = getenv("MEMFINE_RASTER");
+    const int t = e ? atoi(e) : 0;
+    return (t >= 0 && t <= 3) ? t : 0;
+  }();
+  return v;
+}
+
 int hip_status(hipError_t e) { return e == hipSuccess ? MEMFINE_OK : MEMFINE_ERR_HIP; }
 
 GemmArgs gemm_args(const memfine_shape& s, int64_t n, const ChunkBuffers& c) {
@@ -207,6 +236,9 @@ GemmArgs gemm_args(const memfine_shape& s, int64_t n, const ChunkBuffers& c) {
   g.dxp = c.dxp;
   g.dgp = c.dgp;
   g.P = dgate_partials(s.F);
+  g.T_h_bytes = s.T * (int64_t)s.h * elem_bytes(s);
+  g.tile_override = tile_override();
+  g.raster = raster_mode();
   return g;
 }
 

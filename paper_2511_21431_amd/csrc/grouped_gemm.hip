@@ -4,27 +4,38 @@
 // paper's Eq. (4) and its derivative in Eq. (5); Table 2 rows 11-13 name the
 // tensors) is written as
 //     C[m, n] = sum_kk A(m, kk) * B(n, kk)
-// over one expert at a time, with the operands staged into LDS as 128-byte
-// K-rows (64 bf16 or 32 fp32 values) and multiplied by 32x32 MFMA
-// instructions (v_mfma_f32_32x32x16_bf16 / v_mfma_f32_32x32x2f32).
+// over one expert at a time and multiplied by 32x32 MFMA instructions
+// (v_mfma_f32_32x32x16_bf16, or v_mfma_f32_32x32x2f32 on the fp32 path).
 //
-// Two kinds of operand loaders fill the LDS tiles:
-//   RowLoader  operand rows whose K values are contiguous in HBM (activation
-//              rows, weights used as W^T); optionally gathered through the
-//              chunk's row->token table, so the dispatch never materialises
-//              a permuted copy of X or dY.
-//   ColLoader  operands whose K index is the slow HBM dimension (weights used
-//              as W, and both operands of the weight gradients, whose K is
-//              the expert's rows); each thread loads 4 K-rows x 16 bytes and
-//              transposes them in registers before one LDS write per column.
-// Tiles are 128 x 128 per 256-thread workgroup (2 x 2 waves of 64 x 64, i.e.
-// 2 x 2 MFMA blocks per wave), K tiles are double-buffered in LDS with one
-// barrier per K step, and LDS rows are XOR-swizzled in 16-byte units so the
-// MFMA operand reads of 32 consecutive rows hit distinct banks.
+// Operand movement.  Every operand tile goes from HBM straight into LDS with
+// buffer_load ... lds (16 bytes per lane, no staging registers); buffer
+// resources bound each tensor, so rows past the end of a tensor, ragged
+// tails and the K tail of a weight-gradient tile read as zero in hardware.
+// Two LDS layouts serve the two ways an operand can sit in HBM:
+//   K-contiguous  ([row][k], 128-byte K rows): activation rows, weights used
+//                 as W^T.  Rows may be gathered through the chunk's
+//                 row -> token table, so dispatch never materialises a
+//                 permuted copy of X or dY.  Read with ds_read_b128.
+//   K-strided     ([k][row], one HBM row per k): weights used as W, and both
+//                 operands of the weight gradients, whose reduction axis is
+//                 the expert's rows.  Read with two ds_read_b64_tr_b16, which
+//                 transpose 4 K rows x 16 columns across each 16-lane group
+//                 into the K-packed MFMA operand (fp32: a plain 4-byte read).
+// Both layouts XOR-swizzle 16-byte units so that the lanes of one LDS read
+// instruction hit distinct banks.
+//
+// Tiling.  A workgroup is 4 waves (2 x 2) and owns a BM x BN output tile;
+// each wave owns (BM/2) x (BN/2) as (BM/64) x (BN/64) MFMA blocks whose
+// accumulators stay in registers for the whole K loop.  The 256 x 256 tile
+// (128 x 128 per wave) reads each LDS operand byte into 4 MFMAs, which keeps
+// LDS and L2 traffic under the matrix cores' rate; 128 x 128 tiles serve
+// problems whose 256 x 256 grid would leave CUs idle.  K tiles (128 bytes of
+// K per operand row) are double-buffered: the copy of tile k+1 runs while
+// the waves multiply tile k, with one barrier per K step.
 //
 // Scheduling on skewed expert loads: the row-grouped GEMMs (forward FC1/FC2,
 // dgrads) enumerate m-tiles expert after expert from the chunk's offsets, so
-// a cold expert costs only its own ceil(rows/128) tiles; the weight-gradient
+// a cold expert costs only its own ceil(rows/BM) tiles; the weight-gradient
 // GEMMs (K = the expert's rows) visit experts in descending row count, the
 // longest tiles first.
 #include "common.h"
@@ -33,162 +44,304 @@
 namespace memfine {
 namespace {
 
-constexpr int kBM = 128, kBN = 128, kThreads = 256;
-constexpr int kRowBytes = 128;
-constexpr int kTileBytes = (kBM + kBN) * kRowBytes;  // one A + one B stage: 32 KB
+constexpr int kThreads = 256;
+constexpr uint32_t kOOB = 0x80000000u;    // byte offset past every buffer's range
+#ifndef MEMFINE_SCHED_HINTS
+#define MEMFINE_SCHED_HINTS 1
+#endif
+constexpr bool kSchedHints = MEMFINE_SCHED_HINTS;
 
-// byte offset of 16-byte unit `c` (0..7) of LDS tile row `row`
-__device__ __forceinline__ int lds_off(int row, int c) {
-  return row * kRowBytes + ((c ^ ((row ^ (row >> 3)) & 7)) << 4);
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
+
+// Tile shape: BM x BN output per workgroup of WM x WN waves, S LDS stages of
+// KB bytes of K per operand row.
+template <int BM_, int BN_, int WM_, int WN_, int S_, int KB_ = 128> struct Cfg {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, S = S_, KB = KB_;
+  static constexpr int NW = WM * WN, kThreads = 64 * NW;
+  static constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
+  static constexpr int MB = WTM / 32, NB = WTN / 32;  // 32x32 MFMA blocks per wave
+  static constexpr int kStage = (BM + BN) * KB;
+  static constexpr int kLds = S * kStage;
+  static constexpr int kWgPerCu = (160 * 1024) / kLds;
+  static constexpr int kMinWaves = (kWgPerCu * NW + 3) / 4 < 3 ? (kWgPerCu * NW + 3) / 4 : 3;
+};
+using Big = Cfg<256, 256, 2, 2, 2>;
+using Small = Cfg<128, 128, 2, 2, 2>;
+
+// Output tiles of one XCD's resident workgroups should share operand tiles
+// in that XCD's L2.  Workgroup ids are dealt round-robin to the 8 XCDs, so
+// XCD x runs ids x, x + 8, ...; give those ids a contiguous logical range,
+// and walk the logical range in groups of kGroupM m-tiles (all n-tiles of the
+// group before the next group), so that resident workgroups cover a compact
+// block of m-tiles x n-tiles.
+__device__ __forceinline__ int xcd_remap(int id, int n) {
+  const int x = id & 7, slot = id >> 3;
+  const int q = n >> 3, r = n & 7;
+  return x * q + min(x, r) + slot;
+}
+__device__ __forceinline__ void grouped_coords(int logical, int mtn, int ntn, int group, int& mt,
+                                               int& nt) {
+  const int per_group = group * ntn;
+  const int g = logical / per_group;
+  const int first_m = g * group;
+  const int gsz = min(mtn - first_m, group);
+  const int r = logical - g * per_group;
+  mt = first_m + r % gsz;
+  nt = r / gsz;
+}
+// Tile coordinates of workgroup `id` of `n` on an mtn x ntn grid.  raster:
+// 0 = row-major (n-tiles fastest), else XCD-grouped with group size
+// 4 << (raster - 1) m-tiles.
+__device__ __forceinline__ void tile_coords(int raster, int id, int n, int mtn, int ntn, int& mt,
+                                            int& nt) {
+  if (raster == 0) {
+    mt = id / ntn;
+    nt = id % ntn;
+  } else {
+    grouped_coords(xcd_remap(id, n), mtn, ntn, 4 << (raster - 1), mt, nt);
+  }
 }
 
-template <typename T> struct Mfma;
-template <> struct Mfma<bf16_t> {
-  static constexpr int kBK = 64;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  const int32_t n = (int32_t)(bytes < (int64_t)kOOB ? bytes : (int64_t)kOOB - 1);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
+
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t voff,
+                                           uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds, 16, voff, soff, 0, 0);
+}
+
+template <typename T> struct Mma;
+template <> struct Mma<bf16_t> {
   static constexpr int kKStep = 16;
   typedef bf16x8_t Frag;
-  __device__ __forceinline__ static Frag read(const char* lds, int row, int kk, int lane) {
-    const int c = kk * 2 + (lane >> 5);  // 8 K values = one 16-byte unit
-    return *(const bf16x8_t*)(lds + lds_off(row, c));
-  }
   __device__ __forceinline__ static void mma(const Frag& a, const Frag& b, f32x16_t& c) {
     c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
 };
-template <> struct Mfma<float> {
-  static constexpr int kBK = 32;
+template <> struct Mma<float> {
   static constexpr int kKStep = 2;
   typedef float Frag;
-  __device__ __forceinline__ static Frag read(const char* lds, int row, int kk, int lane) {
-    const int kel = kk * 2 + (lane >> 5);
-    return *(const float*)(lds + lds_off(row, kel >> 2) + ((kel & 3) << 2));
-  }
   __device__ __forceinline__ static void mma(const Frag& a, const Frag& b, f32x16_t& c) {
     c = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
   }
 };
 
+// --------------------------------------------------------- K-contiguous
+// LDS tile: ROWS rows x KB bytes (KB = 64 or 128, i.e. U = 4 or 8 units of
+// 16 bytes); unit c of row r sits at unit c ^ sw(r), which puts the 8 rows
+// that one LDS cycle serves on distinct banks.  The direct copy writes 1 KB
+// (1024 / KB rows) per wave instruction: lane l lands at physical unit
+// l % U of row l / U, so it fetches the logical unit (l % U) ^ sw(row).
+template <int KB> __device__ __forceinline__ int kc_sw(int row) {
+  if constexpr (KB == 128) return (row ^ (row >> 3)) & 7;
+  else return (row >> 1) & 3;
+}
+template <int KB> __device__ __forceinline__ int kc_off(int row, int c) {
+  return row * KB + ((c ^ kc_sw<KB>(row)) << 4);
+}
+template <int KB, int ROWS>
+__device__ __forceinline__ bf16x8_t kc_read_bf16(const char* lds, int row0, int kk, int lane) {
+  const int row = row0 + (lane & 31);
+  return *(const bf16x8_t*)(lds + kc_off<KB>(row, kk * 2 + (lane >> 5)));
+}
+template <int KB, int ROWS>
+__device__ __forceinline__ float kc_read_f32(const char* lds, int row0, int kk, int lane) {
+  const int row = row0 + (lane & 31);
+  const int kel = kk * 2 + (lane >> 5);
+  return *(const float*)(lds + kc_off<KB>(row, kel >> 2) + ((kel & 3) << 2));
+}
+
+template <typename T, int ROWS, int NW, int KB> struct KcOp {
+  static constexpr int kReadsPerFrag = 1;
+  static constexpr int U = KB / 16;          // 16-byte units per row
+  static constexpr int RPI = 1024 / KB;      // rows per copy instruction
+  static constexpr int I = ROWS / (RPI * NW);  // copy instructions per wave per K tile
+  static_assert(I * RPI * NW == ROWS, "tile rows must split evenly over the waves");
+  __amdgpu_buffer_rsrc_t rs;
+  uint32_t voff[I];
+  __device__ __forceinline__ static int row_of(int i, int wave, int lane) {
+    return RPI * (i * NW + wave) + lane / U;
+  }
+  // row_byte(row) -> byte offset of the row's first K element, or kOOB
+  template <class F> __device__ __forceinline__ void init(F row_byte, int wave, int lane) {
+#pragma clang loop unroll(full)
+    for (int i = 0; i < I; ++i) {
+      const int row = row_of(i, wave, lane);
+      const uint32_t rb = row_byte(row);
+      voff[i] = rb == kOOB ? kOOB : rb + (uint32_t)((((lane % U) ^ kc_sw<KB>(row)) << 4));
+    }
+  }
+  __device__ __forceinline__ void issue(char* lds, int kt, int wave) const {
+#pragma clang loop unroll(full)
+    for (int i = 0; i < I; ++i) load_lds16(rs, lds + (i * NW + wave) * 1024, voff[i], kt * KB);
+  }
+  __device__ __forceinline__ static typename Mma<T>::Frag read(const char* lds, int row0, int kk,
+                                                               int lane) {
+    if constexpr (sizeof(T) == 2) return kc_read_bf16<KB, ROWS>(lds, row0, kk, lane);
+    else return kc_read_f32<KB, ROWS>(lds, row0, kk, lane);
+  }
+};
+
+// ------------------------------------------------------------ K-strided
+// LDS tile: BK rows (one per k) of ROWS elements (pitch P = ROWS * size);
+// 16-byte unit u of k-row k sits at unit u ^ ks_sw(k).  The swizzle spreads
+// the 4 consecutive k-rows that one transposing read touches over distinct
+// banks.  A copy instruction writes 1 KB = 1024 / P whole k-rows.
+__device__ __forceinline__ int ks_sw(int k) {
+  // k & 3 = 0, 1, 2, 3  ->  units 0, 10, 4, 14 (branch-free)
+  return ((k & 1) * 10) ^ ((k & 2) * 2);
+}
+
+template <typename T, int ROWS, int NW, int KB> struct KsOp {
+  static constexpr int kReadsPerFrag = sizeof(T) == 2 ? 2 : 1;
+  static constexpr int BKE = KB / (int)sizeof(T);  // k-rows per K tile
+  static constexpr int P = ROWS * (int)sizeof(T);
+  static constexpr int KPI = 1024 / P;          // k-rows per copy instruction
+  static constexpr int I = BKE / (KPI * NW);      // copy instructions per wave per K tile
+  static_assert(I * KPI * NW == BKE, "K tile must split evenly over the waves");
+  static constexpr int V = 16 / (int)sizeof(T); // elements per 16-byte unit
+  __amdgpu_buffer_rsrc_t rs;
+  uint32_t voff[I];
+  // lane's k-row (within the K tile) and logical element column of instruction i
+  __device__ __forceinline__ static int k_of(int i, int wave, int lane) {
+    return (i * NW + wave) * KPI + (lane * 16) / P;
+  }
+  __device__ __forceinline__ static int col_of(int i, int wave, int lane) {
+    const int k = k_of(i, wave, lane);
+    const int p = ((lane * 16) % P) >> 4;
+    return (p ^ ks_sw(k)) * V;
+  }
+  __device__ __forceinline__ void issue(char* lds, uint32_t soff, int wave) const {
+#pragma clang loop unroll(full)
+    for (int i = 0; i < I; ++i) load_lds16(rs, lds + (i * NW + wave) * 1024, voff[i], soff);
+  }
+  __device__ __forceinline__ static int phys(int k, int col) {  // byte of element col in k-row
+    const int b = col * (int)sizeof(T);
+    return k * P + ((((b >> 4) ^ ks_sw(k))) << 4) + (b & 15);
+  }
+  __device__ __forceinline__ static typename Mma<T>::Frag read(const char* lds, int col0, int kk,
+                                                               int lane);
+};
+// k-row k, element column col: byte offset inside a K-strided tile of pitch P
+template <int P, int ES>
+__device__ __forceinline__ int ks_phys(int k, int col) {
+  const int b = col * ES;
+  return k * P + ((((b >> 4) ^ ks_sw(k))) << 4) + (b & 15);
+}
+template <int ROWS>
+__device__ __forceinline__ bf16x8_t ks_read_bf16(const char* lds, int col0, int kk, int lane) {
+  // MFMA lane l wants column col0 + l%32 and K values 8*(l/32) .. +7.  In the
+  // 16-lane group G = l/16, source lane j supplies 4 columns starting at
+  // col0 + 16*(G%2) + 4*(j%4) of k-row 16 kk + 8*(G/2) + 4h + j/4; after the
+  // transpose, lane j of the group holds that column's 4 consecutive k.
+  const int j = lane & 15, G = lane >> 4;
+  const int col = col0 + (G & 1) * 16 + 4 * (j & 3);
+  const int k0 = kk * 16 + (G >> 1) * 8 + (j >> 2);
+  const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_s16x4*)(lds + ks_phys<ROWS * 2, 2>(k0, col)));
+  const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_s16x4*)(lds + ks_phys<ROWS * 2, 2>(k0 + 4, col)));
+  return __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+template <int ROWS>
+__device__ __forceinline__ float ks_read_f32(const char* lds, int col0, int kk, int lane) {
+  return *(const float*)(lds + ks_phys<ROWS * 4, 4>(kk * 2 + (lane >> 5), col0 + (lane & 31)));
+}
+template <typename T, int ROWS, int NW, int KB>
+__device__ __forceinline__ typename Mma<T>::Frag KsOp<T, ROWS, NW, KB>::read(const char* lds, int col0,
+                                                                       int kk, int lane) {
+  if constexpr (sizeof(T) == 2) return ks_read_bf16<ROWS>(lds, col0, kk, lane);
+  else return ks_read_f32<ROWS>(lds, col0, kk, lane);
+}
+// --------------------------------------------------------------- compute
+template <class C> struct Accum {
+  f32x16_t v[C::MB][C::NB];
+};
+
+// One K tile: the operand fragments of K step kk+1 are read from LDS while
+// the MFMAs of step kk run (two fragment register sets); scheduling
+// barriers interleave the LDS reads with the MFMAs so that neither waits
+// on the other.
+template <typename T, class C, class OA, class OB>
+__device__ __forceinline__ void mma_tile(const char* As, const char* Bs, Accum<C>& acc, int wm,
+                                         int wn, int lane) {
+  constexpr int KS = C::KB / (int)sizeof(T) / Mma<T>::kKStep;
+  constexpr int kReads = OA::kReadsPerFrag * C::MB + OB::kReadsPerFrag * C::NB;
+  constexpr int kMfma = C::MB * C::NB;
+  typename Mma<T>::Frag a[2][C::MB], b[2][C::NB];
+#pragma clang loop unroll(full)
+  for (int i = 0; i < C::MB; ++i) a[0][i] = OA::read(As, wm * C::WTM + i * 32, 0, lane);
+#pragma clang loop unroll(full)
+  for (int j = 0; j < C::NB; ++j) b[0][j] = OB::read(Bs, wn * C::WTN + j * 32, 0, lane);
+#pragma clang loop unroll(full)
+  for (int kk = 0; kk < KS; ++kk) {
+    const int cu = kk & 1, nx = cu ^ 1;
+    if (kk + 1 < KS) {
+#pragma clang loop unroll(full)
+      for (int i = 0; i < C::MB; ++i) a[nx][i] = OA::read(As, wm * C::WTM + i * 32, kk + 1, lane);
+#pragma clang loop unroll(full)
+      for (int j = 0; j < C::NB; ++j) b[nx][j] = OB::read(Bs, wn * C::WTN + j * 32, kk + 1, lane);
+    }
+#pragma clang loop unroll(full)
+    for (int i = 0; i < C::MB; ++i)
+#pragma clang loop unroll(full)
+      for (int j = 0; j < C::NB; ++j) Mma<T>::mma(a[cu][i], b[cu][j], acc.v[i][j]);
+  }
+  if constexpr (kSchedHints) {
+    // DS reads of step 0, then per step: MFMAs of step kk interleaved with the
+    // reads of step kk+1, then the MFMAs of the last step.
+    __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+#pragma clang loop unroll(full)
+    for (int kk = 0; kk + 1 < KS; ++kk) {
+#pragma clang loop unroll(full)
+      for (int x = 0; x < kMfma; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (x < kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      if (kReads > kMfma) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kMfma, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
+  }
+}
+
+// Tile row of accumulator element i of MFMA block mb; tile column of block nb.
+template <class C> __device__ __forceinline__ int acc_row(int wm, int mb, int i, int lane) {
+  return wm * C::WTM + mb * 32 + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
+}
+template <class C> __device__ __forceinline__ int acc_col(int wn, int nb, int lane) {
+  return wn * C::WTN + nb * 32 + (lane & 31);
+}
+
 struct Tile {
   int e;      // expert
   int m0;     // first output row (row-grouped: chunk row; wgrad: weight row)
   int mrows;  // valid output rows in this tile
-  int n0;     // first output column
+  int n0;     // first output column (FC1: first f)
   int K;      // reduction length
   int r0;     // wgrad: first chunk row of the expert
 };
 
-// ---------------------------------------------------------------- loaders
-// 128 tile rows x 128 bytes; thread q-th unit: idx = tid + 256 q,
-// row = idx >> 3, unit = idx & 7 (8 threads read one row's 128 bytes).
-struct RowLoader {
-  const char* ptr[4];
-  u32x4_t reg[4];
-  __device__ __forceinline__ void set_row(int q, const char* p) { ptr[q] = p; }
-  __device__ __forceinline__ void fetch(int kt) {
-    const int c = threadIdx.x & 7;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (ptr[q]) reg[q] = *(const u32x4_t*)(ptr[q] + (int64_t)kt * kRowBytes + c * 16);
-      else reg[q] = u32x4_t{0u, 0u, 0u, 0u};
-    }
-  }
-  __device__ __forceinline__ void store(char* lds) const {
-    const int c = threadIdx.x & 7;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int row = (threadIdx.x + 256 * q) >> 3;
-      *(u32x4_t*)(lds + lds_off(row, c)) = reg[q];
-    }
-  }
-  __device__ __forceinline__ static int row_of(int q) { return (threadIdx.x + 256 * q) >> 3; }
-};
-
-// Operand with K as the slow dimension.  Thread (ng, kg): ng = tid % NG picks
-// 16 bytes (V elements = V tile rows) of every K row, kg = tid / NG picks K
-// rows 4kg .. 4kg+3 of the K tile.
-template <typename T> struct ColLoader {
-  static constexpr int V = Elem<T>::kVec;
-  static constexpr int NG = 128 / V;
-  u32x4_t reg[4];
-  __device__ __forceinline__ static int ng() { return threadIdx.x % NG; }
-  __device__ __forceinline__ static int kg() { return threadIdx.x / NG; }
-  __device__ __forceinline__ void fetch(const char* const (&p)[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if (p[i]) reg[i] = *(const u32x4_t*)p[i];
-      else reg[i] = u32x4_t{0u, 0u, 0u, 0u};
-    }
-  }
-  __device__ __forceinline__ void store(char* lds) const;
-};
-
-template <> __device__ __forceinline__ void ColLoader<bf16_t>::store(char* lds) const {
-  // 4 K values x 8 columns of bf16 -> per column 8 bytes (4 K values)
-  const int n = ng(), g = kg();
-  const int c = g >> 1, half = (g & 1) * 8;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const uint32_t lo0 = (reg[0][j] & 0xffffu) | (reg[1][j] << 16);
-    const uint32_t lo1 = (reg[2][j] & 0xffffu) | (reg[3][j] << 16);
-    const uint32_t hi0 = (reg[0][j] >> 16) | (reg[1][j] & 0xffff0000u);
-    const uint32_t hi1 = (reg[2][j] >> 16) | (reg[3][j] & 0xffff0000u);
-    const int r0 = n * 8 + 2 * j, r1 = r0 + 1;
-    *(u32x2_t*)(lds + lds_off(r0, c) + half) = u32x2_t{lo0, lo1};
-    *(u32x2_t*)(lds + lds_off(r1, c) + half) = u32x2_t{hi0, hi1};
-  }
+// m-tile bound for the row-grouped grid: sum_e ceil(c_e / BM) <= this.
+inline int row_tiles_bound(int n, int E, int BM) {
+  return (int)(((int64_t)n + (int64_t)E * (BM - 1)) / BM);
 }
-template <> __device__ __forceinline__ void ColLoader<float>::store(char* lds) const {
-  // 4 K values x 4 columns of fp32 -> per column one 16-byte unit
-  const int n = ng(), g = kg();
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int r = n * 4 + j;
-    *(u32x4_t*)(lds + lds_off(r, g)) = u32x4_t{reg[0][j], reg[1][j], reg[2][j], reg[3][j]};
-  }
-}
-
-// --------------------------------------------------------------- compute
-template <typename T>
-__device__ __forceinline__ void mma_tile(const char* As, const char* Bs, f32x16_t (&acc)[2][2],
-                                         int wm, int wn, int lane) {
-  constexpr int KS = Mfma<T>::kBK / Mfma<T>::kKStep;
-#pragma unroll
-  for (int kk = 0; kk < KS; ++kk) {
-    typename Mfma<T>::Frag a[2], b[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      a[i] = Mfma<T>::read(As, wm * 64 + i * 32 + (lane & 31), kk, lane);
-      b[i] = Mfma<T>::read(Bs, wn * 64 + i * 32 + (lane & 31), kk, lane);
-    }
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) Mfma<T>::mma(a[i], b[j], acc[i][j]);
-  }
-}
-
-// Row (within the 128-row tile) of accumulator element i of MFMA block mb.
-__device__ __forceinline__ int acc_row(int wm, int mb, int i, int lane) {
-  return wm * 64 + mb * 32 + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
-}
-__device__ __forceinline__ int acc_col(int wn, int nb, int lane) {
-  return wn * 64 + nb * 32 + (lane & 31);
-}
-
-// m-tile bound for the row-grouped grid: sum_e ceil(c_e / 128) <= this.
-inline int row_tiles_bound(int n, int E) { return (int)(((int64_t)n + (int64_t)E * (kBM - 1)) / kBM); }
 
 // Expert and rows of m-tile `mt` of a row-grouped problem.
+template <int BM>
 __device__ __forceinline__ bool locate_rows(const int32_t* __restrict__ offsets, int E, int mt,
                                             Tile& t) {
   int acc = 0;
   for (int e = 0; e < E; ++e) {
     const int r0 = offsets[e], r1 = offsets[e + 1];
-    const int tiles = (r1 - r0 + kBM - 1) / kBM;
+    const int tiles = (r1 - r0 + BM - 1) / BM;
     if (mt < acc + tiles) {
       t.e = e;
-      t.m0 = r0 + (mt - acc) * kBM;
-      t.mrows = min(kBM, r1 - t.m0);
+      t.m0 = r0 + (mt - acc) * BM;
+      t.mrows = min(BM, r1 - t.m0);
       return true;
     }
     acc += tiles;
@@ -201,93 +354,121 @@ template <typename T> __device__ __forceinline__ const char* cptr(const void* ba
 }
 
 // ================================================================ problems
+// Each problem provides locate (tile of this workgroup), init (buffer
+// resources and per-lane copy offsets), issue (start the direct copies of one
+// K tile into LDS), and epilogue (consume the accumulators).
+
 // Forward FC1 + SwiGLU (and the backward's recompute of it).
 //   A(m, kk) = X[tok(m0 + m), kk]            K = h  (gathered rows)
-//   B(nr, kk) = W1[e, wrow(nr), kk]          tile column nr: waves own 64
-//   columns each = 32 gate rows f and the 32 up rows F + f for the same f, so
-//   every lane holds both halves of its SwiGLU pair.
-template <typename T, bool kRecompute> struct ProbFC1 {
-  RowLoader A, B;
-  static int tiles_n(const GemmArgs& g) { return g.F / 64; }
-  __device__ bool locate(const GemmArgs& g, Tile& t) const {
-    const int ntn = g.F / 64;
-    const int mt = blockIdx.x / ntn, nt = blockIdx.x % ntn;
-    if (!locate_rows(g.offsets, g.E, mt, t)) return false;
-    t.n0 = nt * 64;  // first f of the tile
+//   B(nr, kk) = W1[e, wrow(nr), kk]          each wave's WTN tile columns are
+//   WTN/2 gate rows f followed by the WTN/2 up rows F + f of the same f, so
+//   every lane holds both halves of its SwiGLU pairs (blocks nb, nb + NB/2).
+template <typename T, class C, bool kRecompute> struct ProbFC1 {
+  static constexpr int kHalf = C::WTN / 2;
+  typedef KcOp<T, C::BM, C::NW, C::KB> OA;
+  typedef KcOp<T, C::BN, C::NW, C::KB> OB;
+  OA A;
+  OB B;
+  static int grid(const GemmArgs& g) {
+    return row_tiles_bound(g.n, g.E, C::BM) * ((g.F + C::BN / 2 - 1) / (C::BN / 2));
+  }
+  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t) const {
+    const int ntn = (g.F + C::BN / 2 - 1) / (C::BN / 2);
+    int mt, nt;
+    tile_coords(g.raster, blockIdx.x, gridDim.x, gridDim.x / ntn, ntn, mt, nt);
+    if (!locate_rows<C::BM>(g.offsets, g.E, mt, t)) return false;
+    t.n0 = nt * (C::BN / 2);
     t.K = g.h;
     return true;
   }
-  __device__ void init(const GemmArgs& g, const Tile& t) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r = RowLoader::row_of(q);
-      A.set_row(q, r < t.mrows ? cptr<T>(g.X, (int64_t)g.tok_of_row[t.m0 + r] * g.h) : nullptr);
-      const int f = t.n0 + (r >> 6) * 32 + (r & 31);
-      const int wrow = (r & 32) ? g.F + f : f;
-      B.set_row(q, cptr<T>(g.W1, ((int64_t)t.e * 2 * g.F + wrow) * g.h));
-    }
+  __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
+    A.rs = make_rsrc(g.X, g.T_h_bytes);
+    const int32_t* tok = g.tok_of_row + t.m0;
+    const uint32_t rowb = (uint32_t)g.h * sizeof(T);
+    A.init([&](int r) { return r < t.mrows ? (uint32_t)tok[r] * rowb : kOOB; }, wave, lane);
+    B.rs = make_rsrc(cptr<T>(g.W1, (int64_t)t.e * 2 * g.F * g.h), (int64_t)2 * g.F * g.h * sizeof(T));
+    B.init([&](int r) {
+      const int w = r / C::WTN, q = r % C::WTN;
+      const int f = t.n0 + w * kHalf + (q % kHalf);
+      const int wrow = q >= kHalf ? g.F + f : f;
+      return f < g.F ? (uint32_t)wrow * rowb : kOOB;
+    }, wave, lane);
   }
-  __device__ void fetch(const GemmArgs&, const Tile&, int kt) { A.fetch(kt); B.fetch(kt); }
-  __device__ void store(char* As, char* Bs) const { A.store(As); B.store(Bs); }
-  __device__ void epilogue(const GemmArgs& g, const Tile& t, const f32x16_t (&acc)[2][2], int wm,
-                           int wn, int lane) const {
-    const int f = t.n0 + wn * 32 + (lane & 31);
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int r = acc_row(wm, mb, i, lane);
-        if (r >= t.mrows) continue;
-        const int64_t row = t.m0 + r;
-        const float gate = acc[mb][0][i], up = acc[mb][1][i];
-        const float act = gate * sigmoidf_(gate) * up;
-        if (!kRecompute) {
-          Elem<T>::store((T*)g.a + row * g.F + f, act);
-        } else {
-          T* u = (T*)g.u + row * 2 * g.F;
-          Elem<T>::store(u + f, gate);
-          Elem<T>::store(u + g.F + f, up);
-          Elem<T>::store((T*)g.ag + row * g.F + f, g.gate_of_row[row] * act);
+  __device__ __forceinline__ void issue(const GemmArgs&, const Tile&, int kt, char* As, char* Bs,
+                                        int wave, int) {
+    A.issue(As, kt, wave);
+    B.issue(Bs, kt, wave);
+  }
+  __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
+                                           int wm, int wn, int lane) const {
+#pragma clang loop unroll(full)
+    for (int nb = 0; nb < C::NB / 2; ++nb) {
+      const int f = t.n0 + wn * kHalf + nb * 32 + (lane & 31);
+      if (f >= g.F) continue;
+#pragma clang loop unroll(full)
+      for (int mb = 0; mb < C::MB; ++mb)
+#pragma clang loop unroll(full)
+        for (int i = 0; i < 16; ++i) {
+          const int r = acc_row<C>(wm, mb, i, lane);
+          if (r >= t.mrows) continue;
+          const int64_t row = t.m0 + r;
+          const float gate = acc.v[mb][nb][i], up = acc.v[mb][nb + C::NB / 2][i];
+          const float act = gate * sigmoidf_(gate) * up;
+          if (!kRecompute) {
+            Elem<T>::store((T*)g.a + row * g.F + f, act);
+          } else {
+            T* u = (T*)g.u + row * 2 * g.F;
+            Elem<T>::store(u + f, gate);
+            Elem<T>::store(u + g.F + f, up);
+            Elem<T>::store((T*)g.ag + row * g.F + f, g.gate_of_row[row] * act);
+          }
         }
-      }
+    }
   }
 };
 
 // Forward FC2: y[m, n] = sum_f a[m, f] W2[e, n, f].     K = F
-template <typename T> struct ProbFC2 {
-  RowLoader A, B;
-  static int tiles_n(const GemmArgs& g) { return (g.h + kBN - 1) / kBN; }
-  __device__ bool locate(const GemmArgs& g, Tile& t) const {
-    const int ntn = (g.h + kBN - 1) / kBN;
-    const int mt = blockIdx.x / ntn, nt = blockIdx.x % ntn;
-    if (!locate_rows(g.offsets, g.E, mt, t)) return false;
-    t.n0 = nt * kBN;
+template <typename T, class C> struct ProbFC2 {
+  typedef KcOp<T, C::BM, C::NW, C::KB> OA;
+  typedef KcOp<T, C::BN, C::NW, C::KB> OB;
+  OA A;
+  OB B;
+  static int grid(const GemmArgs& g) {
+    return row_tiles_bound(g.n, g.E, C::BM) * ((g.h + C::BN - 1) / C::BN);
+  }
+  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t) const {
+    const int ntn = (g.h + C::BN - 1) / C::BN;
+    int mt, nt;
+    tile_coords(g.raster, blockIdx.x, gridDim.x, gridDim.x / ntn, ntn, mt, nt);
+    if (!locate_rows<C::BM>(g.offsets, g.E, mt, t)) return false;
+    t.n0 = nt * C::BN;
     t.K = g.F;
     return true;
   }
-  __device__ void init(const GemmArgs& g, const Tile& t) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r = RowLoader::row_of(q);
-      A.set_row(q, r < t.mrows ? cptr<T>(g.a, (int64_t)(t.m0 + r) * g.F) : nullptr);
-      const int n = t.n0 + r;
-      B.set_row(q, n < g.h ? cptr<T>(g.W2, ((int64_t)t.e * g.h + n) * g.F) : nullptr);
-    }
+  __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
+    const uint32_t rowb = (uint32_t)g.F * sizeof(T);
+    A.rs = make_rsrc(cptr<T>(g.a, (int64_t)t.m0 * g.F), (int64_t)t.mrows * rowb);
+    A.init([&](int r) { return r < t.mrows ? (uint32_t)r * rowb : kOOB; }, wave, lane);
+    B.rs = make_rsrc(cptr<T>(g.W2, (int64_t)t.e * g.h * g.F), (int64_t)g.h * rowb);
+    B.init([&](int r) { return t.n0 + r < g.h ? (uint32_t)(t.n0 + r) * rowb : kOOB; }, wave, lane);
   }
-  __device__ void fetch(const GemmArgs&, const Tile&, int kt) { A.fetch(kt); B.fetch(kt); }
-  __device__ void store(char* As, char* Bs) const { A.store(As); B.store(Bs); }
-  __device__ void epilogue(const GemmArgs& g, const Tile& t, const f32x16_t (&acc)[2][2], int wm,
-                           int wn, int lane) const {
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      const int n = t.n0 + acc_col(wn, nb, lane);
+  __device__ __forceinline__ void issue(const GemmArgs&, const Tile&, int kt, char* As, char* Bs,
+                                        int wave, int) {
+    A.issue(As, kt, wave);
+    B.issue(Bs, kt, wave);
+  }
+  __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
+                                           int wm, int wn, int lane) const {
+#pragma clang loop unroll(full)
+    for (int nb = 0; nb < C::NB; ++nb) {
+      const int n = t.n0 + acc_col<C>(wn, nb, lane);
       if (n >= g.h) continue;
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
+#pragma clang loop unroll(full)
+      for (int mb = 0; mb < C::MB; ++mb)
+#pragma clang loop unroll(full)
         for (int i = 0; i < 16; ++i) {
-          const int r = acc_row(wm, mb, i, lane);
-          if (r < t.mrows) Elem<T>::store((T*)g.y + (int64_t)(t.m0 + r) * g.h + n, acc[mb][nb][i]);
+          const int r = acc_row<C>(wm, mb, i, lane);
+          if (r < t.mrows) Elem<T>::store((T*)g.y + (int64_t)(t.m0 + r) * g.h + n, acc.v[mb][nb][i]);
         }
     }
   }
@@ -297,130 +478,154 @@ template <typename T> struct ProbFC2 {
 // fused into the epilogue:
 //   dA[m, f] = sum_o dY[tok(m), o] W2[e, o, f]          K = h
 //   a = silu(u_g) u_u;  da = g dA;  du_g = da u_u silu'(u_g);  du_u = da silu(u_g)
-//   dgp[m, p] = sum over this wave's 64 columns of dA * a
+//   dgp[m, f / 64] = sum over the 64 columns f of one pair of blocks of dA * a
 // du overwrites u in place (each element is read and written by one lane).
-template <typename T> struct ProbFC2Dgrad {
-  RowLoader A;
-  ColLoader<T> B;
-  const char* bbase;  // W2[e] + this thread's column group
-  bool bvalid;
-  static int tiles_n(const GemmArgs& g) { return (g.F + kBN - 1) / kBN; }
-  __device__ bool locate(const GemmArgs& g, Tile& t) const {
-    const int ntn = (g.F + kBN - 1) / kBN;
-    const int mt = blockIdx.x / ntn, nt = blockIdx.x % ntn;
-    if (!locate_rows(g.offsets, g.E, mt, t)) return false;
-    t.n0 = nt * kBN;
+template <typename T, class C> struct ProbFC2Dgrad {
+  typedef KcOp<T, C::BM, C::NW, C::KB> OA;
+  typedef KsOp<T, C::BN, C::NW, C::KB> OB;
+  OA A;
+  OB B;
+  uint32_t b_ktile;  // bytes of W2 per K tile (BK rows)
+  static int grid(const GemmArgs& g) {
+    return row_tiles_bound(g.n, g.E, C::BM) * ((g.F + C::BN - 1) / C::BN);
+  }
+  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t) const {
+    const int ntn = (g.F + C::BN - 1) / C::BN;
+    int mt, nt;
+    tile_coords(g.raster, blockIdx.x, gridDim.x, gridDim.x / ntn, ntn, mt, nt);
+    if (!locate_rows<C::BM>(g.offsets, g.E, mt, t)) return false;
+    t.n0 = nt * C::BN;
     t.K = g.h;
     return true;
   }
-  __device__ void init(const GemmArgs& g, const Tile& t) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r = RowLoader::row_of(q);
-      A.set_row(q, r < t.mrows ? cptr<T>(g.dY, (int64_t)g.tok_of_row[t.m0 + r] * g.h) : nullptr);
+  __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
+    A.rs = make_rsrc(g.dY, g.T_h_bytes);
+    const int32_t* tok = g.tok_of_row + t.m0;
+    const uint32_t rowb = (uint32_t)g.h * sizeof(T);
+    A.init([&](int r) { return r < t.mrows ? (uint32_t)tok[r] * rowb : kOOB; }, wave, lane);
+    const uint32_t ld = (uint32_t)g.F * sizeof(T);  // W2[e] row o holds F values
+    B.rs = make_rsrc(cptr<T>(g.W2, (int64_t)t.e * g.h * g.F), (int64_t)g.h * ld);
+#pragma clang loop unroll(full)
+    for (int i = 0; i < OB::I; ++i) {
+      const int col = t.n0 + OB::col_of(i, wave, lane);
+      B.voff[i] = col < g.F ? (uint32_t)OB::k_of(i, wave, lane) * ld + col * sizeof(T) : kOOB;
     }
-    const int n = t.n0 + ColLoader<T>::ng() * ColLoader<T>::V;
-    bvalid = n < g.F;
-    bbase = cptr<T>(g.W2, (int64_t)t.e * g.h * g.F + n);
+    b_ktile = ld * OB::BKE;
   }
-  __device__ void fetch(const GemmArgs& g, const Tile&, int kt) {
-    A.fetch(kt);
-    const char* p[4];
-    const int k0 = kt * Mfma<T>::kBK + ColLoader<T>::kg() * 4;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) p[i] = bvalid ? bbase + (int64_t)(k0 + i) * g.F * sizeof(T) : nullptr;
-    B.fetch(p);
+  __device__ __forceinline__ void issue(const GemmArgs&, const Tile&, int kt, char* As, char* Bs,
+                                        int wave, int) {
+    A.issue(As, kt, wave);
+    B.issue(Bs, kt * b_ktile, wave);
   }
-  __device__ void store(char* As, char* Bs) const { A.store(As); B.store(Bs); }
-  __device__ void epilogue(const GemmArgs& g, const Tile& t, const f32x16_t (&acc)[2][2], int wm,
-                           int wn, int lane) const {
-    float part[2][16];
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) part[mb][i] = 0.f;
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      const int f = t.n0 + acc_col(wn, nb, lane);
-      if (f >= g.F) continue;
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int r = acc_row(wm, mb, i, lane);
-          if (r >= t.mrows) continue;
-          const int64_t row = t.m0 + r;
-          T* u = (T*)g.u + row * 2 * g.F;
-          const float ug = Elem<T>::load(u + f), uu = Elem<T>::load(u + g.F + f);
-          const float s = sigmoidf_(ug), silu = ug * s;
-          const float dA = acc[mb][nb][i];
-          part[mb][i] = fmaf(dA, silu * uu, part[mb][i]);
-          const float da = g.gate_of_row[row] * dA;
-          Elem<T>::store(u + f, da * uu * s * (1.f + ug * (1.f - s)));
-          Elem<T>::store(u + g.F + f, da * silu);
+  __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
+                                           int wm, int wn, int lane) const {
+#pragma clang loop unroll(full)
+    for (int pb = 0; pb < C::NB / 2; ++pb) {  // pairs of 32-column blocks
+      const int f0 = t.n0 + acc_col<C>(wn, 2 * pb, 0);
+#pragma clang loop unroll(full)
+      for (int mb = 0; mb < C::MB; ++mb) {
+        float part[16];
+#pragma clang loop unroll(full)
+        for (int i = 0; i < 16; ++i) part[i] = 0.f;
+#pragma clang loop unroll(full)
+        for (int h2 = 0; h2 < 2; ++h2) {
+          const int nb = 2 * pb + h2;
+          const int f = t.n0 + acc_col<C>(wn, nb, lane);
+          if (f >= g.F) continue;
+          // read the block's u values first, then compute and write du
+          float ug[16], uu[16], gt[16];
+#pragma clang loop unroll(full)
+          for (int i = 0; i < 16; ++i) {
+            const int r = acc_row<C>(wm, mb, i, lane);
+            const bool in = r < t.mrows;
+            const int64_t row = t.m0 + (in ? r : 0);
+            const T* u = (const T*)g.u + row * 2 * g.F;
+            // unconditional loads (row is clamped into the tile): no branch
+            // splits the batch
+            const float vg = Elem<T>::load(u + f), vu = Elem<T>::load(u + g.F + f);
+            const float vt = g.gate_of_row[row];
+            ug[i] = in ? vg : 0.f;
+            uu[i] = in ? vu : 0.f;
+            gt[i] = in ? vt : 0.f;
+          }
+#pragma clang loop unroll(full)
+          for (int i = 0; i < 16; ++i) {
+            const int r = acc_row<C>(wm, mb, i, lane);
+            const float s = sigmoidf_(ug[i]), silu = ug[i] * s;
+            const float dA = acc.v[mb][nb][i];
+            part[i] = fmaf(dA, silu * uu[i], part[i]);
+            const float da = gt[i] * dA;
+            if (r < t.mrows) {
+              T* u = (T*)g.u + (int64_t)(t.m0 + r) * 2 * g.F;
+              Elem<T>::store(u + f, da * uu[i] * s * (1.f + ug[i] * (1.f - s)));
+              Elem<T>::store(u + g.F + f, da * silu);
+            }
+          }
         }
-    }
-    // sum the partials over the 32 columns held by lanes with equal lane>>5
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float v = part[mb][i];
-#pragma unroll
-        for (int o = 1; o < 32; o <<= 1) v += __shfl_xor(v, o, 64);
-        const int r = acc_row(wm, mb, i, lane);
-        if ((lane & 31) == 0 && r < t.mrows)
-          g.dgp[(int64_t)(t.m0 + r) * g.P + t.n0 / 64 + wn] = v;
+        // sum over the 32 columns held by the lanes with equal lane >> 5
+#pragma clang loop unroll(full)
+        for (int i = 0; i < 16; ++i) {
+          float v = part[i];
+#pragma clang loop unroll(full)
+          for (int o = 1; o < 32; o <<= 1) v += __shfl_xor(v, o, 64);
+          const int r = acc_row<C>(wm, mb, i, lane);
+          if ((lane & 31) == 0 && r < t.mrows && f0 < g.F)
+            g.dgp[(int64_t)(t.m0 + r) * g.P + f0 / 64] = v;
+        }
       }
+    }
   }
 };
 
 // Backward FC1 dgrad: dxp[m, n] = sum_c du[m, c] W1[e, c, n].    K = 2F
-template <typename T> struct ProbFC1Dgrad {
-  RowLoader A;
-  ColLoader<T> B;
-  const char* bbase;
-  bool bvalid;
-  static int tiles_n(const GemmArgs& g) { return (g.h + kBN - 1) / kBN; }
-  __device__ bool locate(const GemmArgs& g, Tile& t) const {
-    const int ntn = (g.h + kBN - 1) / kBN;
-    const int mt = blockIdx.x / ntn, nt = blockIdx.x % ntn;
-    if (!locate_rows(g.offsets, g.E, mt, t)) return false;
-    t.n0 = nt * kBN;
+template <typename T, class C> struct ProbFC1Dgrad {
+  typedef KcOp<T, C::BM, C::NW, C::KB> OA;
+  typedef KsOp<T, C::BN, C::NW, C::KB> OB;
+  OA A;
+  OB B;
+  uint32_t b_ktile;
+  static int grid(const GemmArgs& g) {
+    return row_tiles_bound(g.n, g.E, C::BM) * ((g.h + C::BN - 1) / C::BN);
+  }
+  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t) const {
+    const int ntn = (g.h + C::BN - 1) / C::BN;
+    int mt, nt;
+    tile_coords(g.raster, blockIdx.x, gridDim.x, gridDim.x / ntn, ntn, mt, nt);
+    if (!locate_rows<C::BM>(g.offsets, g.E, mt, t)) return false;
+    t.n0 = nt * C::BN;
     t.K = 2 * g.F;
     return true;
   }
-  __device__ void init(const GemmArgs& g, const Tile& t) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r = RowLoader::row_of(q);
-      A.set_row(q, r < t.mrows ? cptr<T>(g.u, (int64_t)(t.m0 + r) * 2 * g.F) : nullptr);
+  __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
+    const uint32_t rowb = (uint32_t)2 * g.F * sizeof(T);
+    A.rs = make_rsrc(cptr<T>(g.u, (int64_t)t.m0 * 2 * g.F), (int64_t)t.mrows * rowb);
+    A.init([&](int r) { return r < t.mrows ? (uint32_t)r * rowb : kOOB; }, wave, lane);
+    const uint32_t ld = (uint32_t)g.h * sizeof(T);  // W1[e] row c holds h values
+    B.rs = make_rsrc(cptr<T>(g.W1, (int64_t)t.e * 2 * g.F * g.h), (int64_t)2 * g.F * ld);
+#pragma clang loop unroll(full)
+    for (int i = 0; i < OB::I; ++i) {
+      const int col = t.n0 + OB::col_of(i, wave, lane);
+      B.voff[i] = col < g.h ? (uint32_t)OB::k_of(i, wave, lane) * ld + col * sizeof(T) : kOOB;
     }
-    const int n = t.n0 + ColLoader<T>::ng() * ColLoader<T>::V;
-    bvalid = n < g.h;
-    bbase = cptr<T>(g.W1, (int64_t)t.e * 2 * g.F * g.h + n);
+    b_ktile = ld * OB::BKE;
   }
-  __device__ void fetch(const GemmArgs& g, const Tile&, int kt) {
-    A.fetch(kt);
-    const char* p[4];
-    const int k0 = kt * Mfma<T>::kBK + ColLoader<T>::kg() * 4;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) p[i] = bvalid ? bbase + (int64_t)(k0 + i) * g.h * sizeof(T) : nullptr;
-    B.fetch(p);
+  __device__ __forceinline__ void issue(const GemmArgs&, const Tile&, int kt, char* As, char* Bs,
+                                        int wave, int) {
+    A.issue(As, kt, wave);
+    B.issue(Bs, kt * b_ktile, wave);
   }
-  __device__ void store(char* As, char* Bs) const { A.store(As); B.store(Bs); }
-  __device__ void epilogue(const GemmArgs& g, const Tile& t, const f32x16_t (&acc)[2][2], int wm,
-                           int wn, int lane) const {
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      const int n = t.n0 + acc_col(wn, nb, lane);
+  __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
+                                           int wm, int wn, int lane) const {
+#pragma clang loop unroll(full)
+    for (int nb = 0; nb < C::NB; ++nb) {
+      const int n = t.n0 + acc_col<C>(wn, nb, lane);
       if (n >= g.h) continue;
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
+#pragma clang loop unroll(full)
+      for (int mb = 0; mb < C::MB; ++mb)
+#pragma clang loop unroll(full)
         for (int i = 0; i < 16; ++i) {
-          const int r = acc_row(wm, mb, i, lane);
-          if (r < t.mrows) Elem<T>::store((T*)g.dxp + (int64_t)(t.m0 + r) * g.h + n, acc[mb][nb][i]);
+          const int r = acc_row<C>(wm, mb, i, lane);
+          if (r < t.mrows) Elem<T>::store((T*)g.dxp + (int64_t)(t.m0 + r) * g.h + n, acc.v[mb][nb][i]);
         }
     }
   }
@@ -429,153 +634,253 @@ template <typename T> struct ProbFC1Dgrad {
 // Weight gradients.  Expert e's rows [r0, r0 + K) are the reduction axis:
 //   FC2: dW2[e, m, n] (+)= sum_r dY[tok(r), m] * ag[r, n]     M = h,  N = F
 //   FC1: dW1[e, m, n] (+)= sum_r du[r, m] * X[tok(r), n]      M = 2F, N = h
-// Both operands are ColLoaders; tile (rank, mt, nt) with experts visited in
-// descending row count.
-template <typename T, bool kFC1> struct ProbWgrad {
-  ColLoader<T> A, B;
-  const char* abase;
-  const char* bbase;
-  bool avalid, bvalid;
+// Both operands are K-strided; the token-gathered one (dY for FC2, X for FC1)
+// computes its per-lane row offsets for every K tile from the row -> token
+// table, one tile ahead.  Tiles (rank, mt, nt) visit experts in descending
+// row count.
+template <typename T, class C, bool kFC1> struct ProbWgrad {
+  typedef KsOp<T, C::BM, C::NW, C::KB> OA;
+  typedef KsOp<T, C::BN, C::NW, C::KB> OB;
+  static constexpr int IG = kFC1 ? OB::I : OA::I;  // copy instructions of the gathered operand
+  OA A;
+  OB B;
+  static constexpr int D = C::S - 1;              // token prefetch distance (K tiles)
+  uint32_t colb[IG];         // gathered operand: byte of this lane's column in a row
+  int32_t tok[D][IG];        // gathered operand: tokens of the next D K tiles' rows
   __host__ __device__ static int M(const GemmArgs& g) { return kFC1 ? 2 * g.F : g.h; }
   __host__ __device__ static int N(const GemmArgs& g) { return kFC1 ? g.h : g.F; }
-  static int tiles(const GemmArgs& g) {
-    return g.E * ((M(g) + kBM - 1) / kBM) * ((N(g) + kBN - 1) / kBN);
+  static int grid(const GemmArgs& g) {
+    return g.E * ((M(g) + C::BM - 1) / C::BM) * ((N(g) + C::BN - 1) / C::BN);
   }
-  __device__ bool locate(const GemmArgs& g, Tile& t) const {
-    const int mtn = (M(g) + kBM - 1) / kBM, ntn = (N(g) + kBN - 1) / kBN;
+  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t) const {
+    const int mtn = (M(g) + C::BM - 1) / C::BM, ntn = (N(g) + C::BN - 1) / C::BN;
     const int per = mtn * ntn;
-    const int rank = blockIdx.x / per, rem = blockIdx.x % per;
+    // experts in descending row count; within an expert, XCD-grouped tiles
+    const int rank = blockIdx.x / per;
+    int mt, nt;
+    tile_coords(g.raster, blockIdx.x - rank * per, per, mtn, ntn, mt, nt);
     t.e = g.order[rank];
     t.r0 = g.offsets[t.e];
     t.K = g.offsets[t.e + 1] - t.r0;
     if (t.K == 0 && g.accumulate) return false;  // nothing to add
-    t.m0 = (rem / ntn) * kBM;
-    t.n0 = (rem % ntn) * kBN;
-    t.mrows = min(kBM, M(g) - t.m0);
+    t.m0 = mt * C::BM;
+    t.n0 = nt * C::BN;
+    t.mrows = min(C::BM, M(g) - t.m0);
     return true;
   }
-  __device__ void init(const GemmArgs& g, const Tile& t) {
-    const int ma = t.m0 + ColLoader<T>::ng() * ColLoader<T>::V;
-    const int nb = t.n0 + ColLoader<T>::ng() * ColLoader<T>::V;
-    avalid = ma < M(g);
-    bvalid = nb < N(g);
-    abase = kFC1 ? cptr<T>(g.u, ma) : cptr<T>(g.dY, ma);
-    bbase = kFC1 ? cptr<T>(g.X, nb) : cptr<T>(g.ag, nb);
+  // tokens of K tile kt's rows for this lane's copy instructions (-1: past K)
+  __device__ __forceinline__ void load_tokens(const GemmArgs& g, const Tile& t, int kt, int wave,
+                                              int lane, int32_t (&dst)[IG]) {
+#pragma clang loop unroll(full)
+    for (int i = 0; i < IG; ++i) {
+      const int k = kt * OA::BKE + (kFC1 ? OB::k_of(i, wave, lane) : OA::k_of(i, wave, lane));
+      const int32_t v = g.tok_of_row[t.r0 + min(k, t.K - 1)];
+      dst[i] = k < t.K ? v : -1;
+    }
   }
-  __device__ void fetch(const GemmArgs& g, const Tile& t, int kt) {
-    const char* pa[4];
-    const char* pb[4];
-    const int k0 = kt * Mfma<T>::kBK + ColLoader<T>::kg() * 4;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int kk = k0 + i;
-      const bool in = kk < t.K;
-      const int row = t.r0 + (in ? kk : 0);
-      if (kFC1) {
-        pa[i] = (in && avalid) ? abase + (int64_t)row * 2 * g.F * sizeof(T) : nullptr;
-        pb[i] = (in && bvalid) ? bbase + (int64_t)g.tok_of_row[row] * g.h * sizeof(T) : nullptr;
-      } else {
-        pa[i] = (in && avalid) ? abase + (int64_t)g.tok_of_row[row] * g.h * sizeof(T) : nullptr;
-        pb[i] = (in && bvalid) ? bbase + (int64_t)row * g.F * sizeof(T) : nullptr;
+  // the non-gathered operand (rows r0 .. r0+K of u for FC1, of ag for FC2) is
+  // re-based at every K tile, so its offsets stay small for any row count
+  __device__ __forceinline__ int ldp(const GemmArgs& g) const { return kFC1 ? 2 * g.F : g.F; }
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t plain_rsrc(const GemmArgs& g, const Tile& t,
+                                                               int kt) const {
+    const int k0 = kt * OA::BKE;
+    const int rows = min(OA::BKE, t.K - k0);
+    return make_rsrc(cptr<T>(kFC1 ? g.u : g.ag, (int64_t)(t.r0 + k0) * ldp(g)),
+                     (int64_t)rows * ldp(g) * sizeof(T));
+  }
+  __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
+    const uint32_t ldpb = (uint32_t)ldp(g) * sizeof(T);
+    const int pcol0 = kFC1 ? t.m0 : t.n0;
+    const int plim = kFC1 ? M(g) : N(g);
+    const __amdgpu_buffer_rsrc_t grs = make_rsrc(kFC1 ? g.X : g.dY, g.T_h_bytes);
+    const int gcol0 = kFC1 ? t.n0 : t.m0;
+    const int glim = kFC1 ? N(g) : M(g);
+    if (kFC1) {
+      B.rs = grs;
+#pragma clang loop unroll(full)
+      for (int i = 0; i < OA::I; ++i) {
+        const int col = pcol0 + OA::col_of(i, wave, lane);
+        A.voff[i] = col < plim ? (uint32_t)OA::k_of(i, wave, lane) * ldpb + col * sizeof(T) : kOOB;
+      }
+#pragma clang loop unroll(full)
+      for (int i = 0; i < IG; ++i) {
+        const int col = gcol0 + OB::col_of(i, wave, lane);
+        colb[i] = col < glim ? col * sizeof(T) : kOOB;
+      }
+    } else {
+      A.rs = grs;
+#pragma clang loop unroll(full)
+      for (int i = 0; i < OB::I; ++i) {
+        const int col = pcol0 + OB::col_of(i, wave, lane);
+        B.voff[i] = col < plim ? (uint32_t)OB::k_of(i, wave, lane) * ldpb + col * sizeof(T) : kOOB;
+      }
+#pragma clang loop unroll(full)
+      for (int i = 0; i < IG; ++i) {
+        const int col = gcol0 + OA::col_of(i, wave, lane);
+        colb[i] = col < glim ? col * sizeof(T) : kOOB;
       }
     }
-    A.fetch(pa);
-    B.fetch(pb);
+#pragma clang loop unroll(full)
+    for (int d = 0; d < D; ++d) load_tokens(g, t, d, wave, lane, tok[d]);
   }
-  __device__ void store(char* As, char* Bs) const { A.store(As); B.store(Bs); }
-  __device__ void epilogue(const GemmArgs& g, const Tile& t, const f32x16_t (&acc)[2][2], int wm,
-                           int wn, int lane) const {
+  __device__ __forceinline__ void issue(const GemmArgs& g, const Tile& t, int kt, char* As,
+                                        char* Bs, int wave, int lane) {
+    const uint32_t rowb = (uint32_t)g.h * sizeof(T);
+    uint32_t* gv = kFC1 ? B.voff : A.voff;
+#pragma clang loop unroll(full)
+    for (int i = 0; i < IG; ++i)
+      gv[i] = (tok[0][i] < 0 || colb[i] == kOOB) ? kOOB : (uint32_t)tok[0][i] * rowb + colb[i];
+    if (kFC1) A.rs = plain_rsrc(g, t, kt);
+    else B.rs = plain_rsrc(g, t, kt);
+    A.issue(As, 0, wave);
+    B.issue(Bs, 0, wave);
+#pragma clang loop unroll(full)
+    for (int d = 0; d + 1 < D; ++d)
+#pragma clang loop unroll(full)
+      for (int i = 0; i < IG; ++i) tok[d][i] = tok[d + 1][i];
+    load_tokens(g, t, kt + D, wave, lane, tok[D - 1]);  // D tiles ahead
+  }
+  __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
+                                           int wm, int wn, int lane) const {
     float* dW = (kFC1 ? g.dW1 : g.dW2) + (int64_t)t.e * M(g) * N(g);
     const int Nn = N(g);
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      const int n = t.n0 + acc_col(wn, nb, lane);
-      if (n >= Nn) continue;
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
+    // all loads of a block before its stores: the old values are read in one
+    // batch instead of one load-add-store round trip per element
+#pragma clang loop unroll(full)
+    for (int nb = 0; nb < C::NB; ++nb) {
+      const int n = t.n0 + acc_col<C>(wn, nb, lane);
+      const bool nin = n < Nn;
+#pragma clang loop unroll(full)
+      for (int mb = 0; mb < C::MB; ++mb) {
+        float old[16];
+#pragma clang loop unroll(full)
         for (int i = 0; i < 16; ++i) {
-          const int r = acc_row(wm, mb, i, lane);
-          if (r >= t.mrows) continue;
-          float* p = dW + (int64_t)(t.m0 + r) * Nn + n;
-          *p = g.accumulate ? *p + acc[mb][nb][i] : acc[mb][nb][i];
+          const int r = acc_row<C>(wm, mb, i, lane);
+          const bool in = nin && r < t.mrows;
+          const float v = g.accumulate ? dW[(int64_t)(t.m0 + (in ? r : 0)) * Nn + (in ? n : t.n0)] : 0.f;
+          old[i] = in ? v : 0.f;
         }
+#pragma clang loop unroll(full)
+        for (int i = 0; i < 16; ++i) {
+          const int r = acc_row<C>(wm, mb, i, lane);
+          if (nin && r < t.mrows) dW[(int64_t)(t.m0 + r) * Nn + n] = old[i] + acc.v[mb][nb][i];
+        }
+      }
     }
   }
 };
 
 // ------------------------------------------------------------------ kernel
-template <typename T, class P>
-__global__ __launch_bounds__(kThreads, 2) void grouped_gemm_kernel(GemmArgs g) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * kTileBytes];
+// s_waitcnt vmcnt(N): at most N vector-memory loads of this wave in flight
+template <int N> __device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit counter");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// K loop over an S-stage ring of LDS tiles.  Tile kt+S-1 is copied into the
+// stage that held tile kt-1 while the waves multiply tile kt.  Before tile
+// kt is used, each wave waits until only the copies of the tiles issued
+// after it may still be in flight (loads retire in order), then a barrier
+// publishes every wave's copies and also certifies that all waves are done
+// with tile kt-1, whose stage the next copy overwrites.
+template <typename T, class C, class P>
+__global__ __launch_bounds__(C::kThreads, C::kMinWaves)
+__attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_gemm_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(1024))) char smem[C::kLds];
   P p;
   Tile t;
   if (!p.locate(g, t)) return;
-  p.init(g, t);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w >> 1, wn = w & 1;
-  f32x16_t acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
-  const int nk = (t.K + Mfma<T>::kBK - 1) / Mfma<T>::kBK;
-  if (nk > 0) {
-    p.fetch(g, t, 0);
-    p.store(smem, smem + kBM * kRowBytes);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w / C::WN, wn = w % C::WN;
+  p.init(g, t, w, lane);
+  Accum<C> acc;
+#pragma clang loop unroll(full)
+  for (int i = 0; i < C::MB; ++i)
+#pragma clang loop unroll(full)
+    for (int j = 0; j < C::NB; ++j)
+#pragma clang loop unroll(full)
+      for (int q = 0; q < 16; ++q) acc.v[i][j][q] = 0.f;
+  constexpr int kCopies = P::OA::I + P::OB::I;  // copy instructions per wave per K tile
+  constexpr int BKE = C::KB / (int)sizeof(T);  // K per tile
+  const int nk = (t.K + BKE - 1) / BKE;
+#pragma clang loop unroll(full)
+  for (int j = 0; j < C::S - 1; ++j) {
+    char* st = smem + j * C::kStage;
+    if (j < nk) p.issue(g, t, j, st, st + C::BM * C::KB, w, lane);
+  }
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + C::S - 2 < nk) wait_vm<(C::S - 2) * kCopies>();
+    else wait_vm<0>();
     __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      char* cur = smem + (kt & 1) * kTileBytes;
-      char* nxt = smem + ((kt + 1) & 1) * kTileBytes;
-      if (kt + 1 < nk) p.fetch(g, t, kt + 1);
-      mma_tile<T>(cur, cur + kBM * kRowBytes, acc, wm, wn, lane);
-      if (kt + 1 < nk) p.store(nxt, nxt + kBM * kRowBytes);
-      __syncthreads();
+    if (kt + C::S - 1 < nk) {
+      char* st = smem + ((kt + C::S - 1) % C::S) * C::kStage;
+      p.issue(g, t, kt + C::S - 1, st, st + C::BM * C::KB, w, lane);
     }
+    char* cur = smem + (kt % C::S) * C::kStage;
+    mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
   }
   p.epilogue(g, t, acc, wm, wn, lane);
 }
 
-template <class PB, class PF>
-hipError_t launch_grid(const GemmArgs& g, int blocks, hipStream_t s) {
+template <template <typename, class> class PT, class C>
+hipError_t launch_cfg(const GemmArgs& g, hipStream_t s) {
+  const int blocks = PT<float, C>::grid(g);
   if (blocks <= 0) return hipSuccess;
-  if (g.dtype == 0) grouped_gemm_kernel<bf16_t, PB><<<blocks, kThreads, 0, s>>>(g);
-  else grouped_gemm_kernel<float, PF><<<blocks, kThreads, 0, s>>>(g);
+  if (g.dtype == 0)
+    grouped_gemm_kernel<bf16_t, C, PT<bf16_t, C>><<<blocks, C::kThreads, 0, s>>>(g);
+  else
+    grouped_gemm_kernel<float, Small, PT<float, Small>><<<PT<float, Small>::grid(g), Small::kThreads,
+                                                          0, s>>>(g);
   return hipGetLastError();
 }
 
+// Workgroup-rounds a grid of `tiles` tiles takes on the whole chip.
+inline double rounds(int tiles, int per_cu) {
+  const int slots = 256 * per_cu;
+  return (double)((tiles + slots - 1) / slots);
+}
+
+using Big8 = Cfg<256, 256, 2, 4, 2>;        // 8 waves of 128 x 64
+using Big8S4 = Cfg<256, 256, 2, 4, 4, 64>;  // half-depth K tiles, 4 stages
+using Big8S5 = Cfg<256, 256, 2, 4, 5, 64>;  // half-depth K tiles, 5 stages
+using SmallS4 = Cfg<128, 128, 2, 2, 4, 64>;
+using SmallS3 = Cfg<128, 128, 2, 2, 3, 64>;
+
+// Pick the tile shape.  The 256 x 256 tile on 8 waves (one workgroup per CU,
+// two waves per SIMD, 128 x 64 per wave) measured fastest on every workload
+// shape here, from 8k to 65k slots and C = 1..4; the 128 x 128 tile (two
+// workgroups per CU) only serves grids too small to give most CUs a tile.
+template <template <typename, class> class PT>
+hipError_t launch_auto(const GemmArgs& g, hipStream_t s) {
+  if (g.dtype != 0) return launch_cfg<PT, Small>(g, s);
+  switch (g.tile_override) {
+    case 1: return launch_cfg<PT, Small>(g, s);
+    case 2: return launch_cfg<PT, Big>(g, s);
+    case 3: return launch_cfg<PT, Big8>(g, s);
+    case 4: return launch_cfg<PT, Big8S4>(g, s);
+    case 5: return launch_cfg<PT, Big8S5>(g, s);
+    case 6: return launch_cfg<PT, SmallS4>(g, s);
+    case 7: return launch_cfg<PT, SmallS3>(g, s);
+    default: break;
+  }
+  if (PT<float, Big8>::grid(g) >= 128) return launch_cfg<PT, Big8>(g, s);
+  return launch_cfg<PT, Small>(g, s);
+}
+
+template <typename T, class C> using FC1Fwd = ProbFC1<T, C, false>;
+template <typename T, class C> using FC1Rec = ProbFC1<T, C, true>;
+template <typename T, class C> using FC2W = ProbWgrad<T, C, false>;
+template <typename T, class C> using FC1W = ProbWgrad<T, C, true>;
+
 }  // namespace
 
-int dgate_partials(int F) { return 2 * ((F + kBN - 1) / kBN); }
+int dgate_partials(int F) { return (F + 63) / 64; }
 
-hipError_t launch_fc1_fwd(const GemmArgs& g, hipStream_t s) {
-  return launch_grid<ProbFC1<bf16_t, false>, ProbFC1<float, false>>(
-      g, row_tiles_bound(g.n, g.E) * (g.F / 64), s);
-}
-hipError_t launch_fc1_recompute(const GemmArgs& g, hipStream_t s) {
-  return launch_grid<ProbFC1<bf16_t, true>, ProbFC1<float, true>>(
-      g, row_tiles_bound(g.n, g.E) * (g.F / 64), s);
-}
-hipError_t launch_fc2_fwd(const GemmArgs& g, hipStream_t s) {
-  return launch_grid<ProbFC2<bf16_t>, ProbFC2<float>>(
-      g, row_tiles_bound(g.n, g.E) * ((g.h + kBN - 1) / kBN), s);
-}
-hipError_t launch_fc2_dgrad(const GemmArgs& g, hipStream_t s) {
-  return launch_grid<ProbFC2Dgrad<bf16_t>, ProbFC2Dgrad<float>>(
-      g, row_tiles_bound(g.n, g.E) * ((g.F + kBN - 1) / kBN), s);
-}
-hipError_t launch_fc1_dgrad(const GemmArgs& g, hipStream_t s) {
-  return launch_grid<ProbFC1Dgrad<bf16_t>, ProbFC1Dgrad<float>>(
-      g, row_tiles_bound(g.n, g.E) * ((g.h + kBN - 1) / kBN), s);
-}
-hipError_t launch_fc2_wgrad(const GemmArgs& g, hipStream_t s) {
-  return launch_grid<ProbWgrad<bf16_t, false>, ProbWgrad<float, false>>(
-      g, ProbWgrad<float, false>::tiles(g), s);
-}
-hipError_t launch_fc1_wgrad(const GemmArgs& g, hipStream_t s) {
-  return launch_grid<ProbWgrad<bf16_t, true>, ProbWgrad<float, true>>(
-      g, ProbWgrad<float, true>::tiles(g), s);
-}
+hipError_t launch_fc1_fwd(const GemmArgs& g, hipStream_t s) { return launch_auto<FC1Fwd>(g, s); }
+hipError_t launch_fc1_recompute(const GemmArgs& g, hipStream_t s) { return launch_auto<FC1Rec>(g, s); }
+hipError_t launch_fc2_fwd(const GemmArgs& g, hipStream_t s) { return launch_auto<ProbFC2>(g, s); }
+hipError_t launch_fc2_dgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<ProbFC2Dgrad>(g, s); }
+hipError_t launch_fc1_dgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<ProbFC1Dgrad>(g, s); }
+hipError_t launch_fc2_wgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<FC2W>(g, s); }
+hipError_t launch_fc1_wgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<FC1W>(g, s); }
 
 }  // namespace memfine

@@ -63,6 +63,9 @@ struct GemmArgs {
   float* dW1;        // [E, 2F, h]
   float* dW2;        // [E, h, F]
   int accumulate;    // wgrad: 1 = add into dW, 0 = overwrite
+  int64_t T_h_bytes; // bytes of X (and of dY): T * h * element size
+  int tile_override; // 0: choose the tile shape per problem; else a fixed shape
+  int raster;        // tile traversal: 0 row-major, 1..3 XCD-grouped (group 4, 8, 16)
 };
 
 int dgate_partials(int F);
