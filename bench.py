@@ -53,6 +53,8 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target duration of the oracle sample")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run one plain 1 GiB device copy first (reference for HBM counters)")
     return ap.parse_args()
 
 
@@ -118,6 +120,13 @@ def main():
     dW2 = torch.empty((w.E, w.h, w.F), dtype=torch.float32, device="cuda")
     dg = torch.empty((w.T, w.k), dtype=torch.float32, device="cuda")
     work = torch.zeros(w.E + 1, dtype=torch.int32, device="cuda")
+    if args.calibrate_copy:
+        # an elementwise pass over 1 GiB (reads 1 GiB, writes 1 GiB) whose
+        # kernel name (neg) is unique in this process
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)
+        del src, dst
     torch.cuda.synchronize()
 
     def step(C_fixed=None, allocator=None):

@@ -13,7 +13,9 @@
  * ---------------------------------------
  * - Pointers named d_* are device pointers, h_* host pointers.  Every buffer
  *   is owned by the caller; the library keeps no state between calls except a
- *   lazily created per-process profiling table.
+ *   lazily created per-process profiling table and, for calls made with a
+ *   NULL allocator, one lazily created stream-ordered memory pool per device
+ *   (its freed chunk memory is kept for reuse until the process ends).
  * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *   Device work is enqueued asynchronously on it; only memfine_count and
  *   memfine_profile_end synchronise (with the stream / the recorded events).
@@ -166,7 +168,9 @@ int64_t memfine_workspace_bytes(const memfine_shape* shape, int32_t chunks, int3
  * F_w = combine(expert(dispatch(.))) of Eq. (4) on tokens
  * [floor(i*T/C), floor((i+1)*T/C)).  Every chunk's buffers are allocated
  * before and released after its kernels.  Nothing is kept for the backward.
- * Y is overwritten.  `chunks` >= 1 (chunks > T behaves like T).
+ * Y is overwritten.  `chunks` >= 1 (chunks > T behaves like T).  A slot whose
+ * id lies outside [0, E) is dropped: it contributes nothing to Y (and, in the
+ * backward, nothing to dX or dW; its dgates entry is 0).
  */
 int memfine_moe_fwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
                     const int32_t* d_idx, const float* d_gates, const void* d_W1,
