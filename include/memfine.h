@@ -204,13 +204,14 @@ const char* memfine_status_str(int status);
 #define MEMFINE_K_FC1         2   /* forward FC1 + SwiGLU                    */
 #define MEMFINE_K_FC2         3   /* forward FC2                             */
 #define MEMFINE_K_COMBINE     4
-#define MEMFINE_K_FC1_RECOMP  5   /* backward: FC1 recompute (u and g*a)      */
-#define MEMFINE_K_FC2_DGRAD   6   /* dA = dY W2 with fused SwiGLU backward   */
+#define MEMFINE_K_FC1_RECOMP  5   /* backward: FC1 recompute + SwiGLU bwd    */
+#define MEMFINE_K_FC2_DGRAD   6   /* backward: dA = dY W2                    */
 #define MEMFINE_K_FC2_WGRAD   7
 #define MEMFINE_K_FC1_WGRAD   8
 #define MEMFINE_K_FC1_DGRAD   9
 #define MEMFINE_K_UNPERMUTE  10   /* dX sum over slots and gate gradient     */
-#define MEMFINE_K_NUM        11
+#define MEMFINE_K_FC1_BWD    11   /* FC1 dgrad and FC1 wgrad in one launch   */
+#define MEMFINE_K_NUM        12
 
 typedef struct memfine_kernel_stat {
   int64_t launches;

@@ -21,7 +21,7 @@ BF16, F32 = 0, 1
 PASS_FWD, PASS_BWD = 0, 1
 
 KERNELS = ["count", "dispatch", "fc1", "fc2", "combine", "fc1_recompute", "fc2_dgrad",
-           "fc2_wgrad", "fc1_wgrad", "fc1_dgrad", "unpermute"]
+           "fc2_wgrad", "fc1_wgrad", "fc1_dgrad", "unpermute", "fc1_dgrad_wgrad"]
 
 
 class MemfineError(RuntimeError):

@@ -216,6 +216,16 @@ int raster_mode() {
   return v;
 }
 
+// MEMFINE_PAIR=1 runs the FC1 dgrad and FC1 wgrad of the backward in one
+// launch (default 0: two launches).
+bool pair_launches() {
+  static const bool v = [] {
+    const char* e = getenv("MEMFINE_PAIR");
+    return e && atoi(e) == 1;
+  }();
+  return v;
+}
+
 int hip_status(hipError_t e) { return e == hipSuccess ? MEMFINE_OK : MEMFINE_ERR_HIP; }
 
 GemmArgs gemm_args(const memfine_shape& s, int64_t n, const ChunkBuffers& c) {
@@ -486,30 +496,39 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
       KernelTimer kt(MEMFINE_K_DISPATCH, s, 0.0, dispatch_work(n).bytes);
       err = launch_dispatch(d_idx, d_gates, t0 * S.k, (int)n, S.E, S.k, cb.m, s);
     }
-    if (err == hipSuccess) {  // recompute F_w(X_i): u and g * a
-      KernelTimer kt(MEMFINE_K_FC1_RECOMP, s, 4.0 * nd * hF,
-                     es * (td * S.h + 2.0 * Ed * hF + 3.0 * nd * S.F));
+    // algorithmic work of the backward GEMMs (flops, bytes)
+    const Work w_fc2d = {2.0 * nd * hF, es * (td * S.h + Ed * hF + nd * S.F)};
+    const Work w_rec = {4.0 * nd * hF,
+                        es * (td * S.h + 2.0 * Ed * hF + 4.0 * nd * S.F) + 4.0 * nd * g.P};
+    const Work w_fc2w = {2.0 * nd * hF, es * (td * S.h + nd * S.F) + dw_rmw * Ed * hF};
+    const Work w_fc1w = {4.0 * nd * hF, es * (2.0 * nd * S.F + td * S.h) + 2.0 * dw_rmw * Ed * hF};
+    const Work w_fc1d = {4.0 * nd * hF, es * (2.0 * nd * S.F + 2.0 * Ed * hF + nd * S.h)};
+    if (err == hipSuccess) {  // dA = dY W2 of the chunk's rows (into ag)
+      KernelTimer kt(MEMFINE_K_FC2_DGRAD, s, w_fc2d.flops, w_fc2d.bytes);
+      err = launch_fc2_dgrad(g, s);
+    }
+    if (err == hipSuccess) {  // recompute F_w(X_i)'s FC1; SwiGLU backward: du, g * a, dg partials
+      KernelTimer kt(MEMFINE_K_FC1_RECOMP, s, w_rec.flops, w_rec.bytes);
       err = launch_fc1_recompute(g, s);
     }
     if (err == hipSuccess) {
-      KernelTimer kt(MEMFINE_K_FC2_DGRAD, s, 2.0 * nd * hF,
-                     es * (td * S.h + Ed * hF + 4.0 * nd * S.F) + 4.0 * nd * g.P);
-      err = launch_fc2_dgrad(g, s);
-    }
-    if (err == hipSuccess) {
-      KernelTimer kt(MEMFINE_K_FC2_WGRAD, s, 2.0 * nd * hF,
-                     es * (td * S.h + nd * S.F) + dw_rmw * Ed * hF);
+      KernelTimer kt(MEMFINE_K_FC2_WGRAD, s, w_fc2w.flops, w_fc2w.bytes);
       err = launch_fc2_wgrad(g, s);
     }
-    if (err == hipSuccess) {
-      KernelTimer kt(MEMFINE_K_FC1_WGRAD, s, 4.0 * nd * hF,
-                     es * (2.0 * nd * S.F + td * S.h) + 2.0 * dw_rmw * Ed * hF);
-      err = launch_fc1_wgrad(g, s);
-    }
-    if (err == hipSuccess) {
-      KernelTimer kt(MEMFINE_K_FC1_DGRAD, s, 4.0 * nd * hF,
-                     es * (2.0 * nd * S.F + 2.0 * Ed * hF + nd * S.h));
-      err = launch_fc1_dgrad(g, s);
+    if (pair_launches()) {
+      if (err == hipSuccess) {
+        KernelTimer kt(MEMFINE_K_FC1_BWD, s, w_fc1d.flops + w_fc1w.flops, w_fc1d.bytes + w_fc1w.bytes);
+        err = launch_fc1_dgrad_wgrad(g, s);
+      }
+    } else {
+      if (err == hipSuccess) {
+        KernelTimer kt(MEMFINE_K_FC1_WGRAD, s, w_fc1w.flops, w_fc1w.bytes);
+        err = launch_fc1_wgrad(g, s);
+      }
+      if (err == hipSuccess) {
+        KernelTimer kt(MEMFINE_K_FC1_DGRAD, s, w_fc1d.flops, w_fc1d.bytes);
+        err = launch_fc1_dgrad(g, s);
+      }
     }
     if (err == hipSuccess) {
       KernelTimer kt(MEMFINE_K_UNPERMUTE, s, nd * S.h,

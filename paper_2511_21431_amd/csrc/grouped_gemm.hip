@@ -289,7 +289,7 @@ __device__ __forceinline__ void mma_tile(const char* As, const char* Bs, Accum<C
 #pragma clang loop unroll(full)
     for (int i = 0; i < C::MB; ++i)
 #pragma clang loop unroll(full)
-      for (int j = 0; j < C::NB; ++j) Mma<T>::mma(a[cu][i], b[cu][j], acc.v[i][j]);
+      for (int j = 0; j < C::NB; ++j) Mma<T>::mma(b[cu][j], a[cu][i], acc.v[i][j]);
   }
   if constexpr (kSchedHints) {
     // DS reads of step 0, then per step: MFMAs of step kk interleaved with the
@@ -308,12 +308,22 @@ __device__ __forceinline__ void mma_tile(const char* As, const char* Bs, Accum<C
   }
 }
 
-// Tile row of accumulator element i of MFMA block mb; tile column of block nb.
-template <class C> __device__ __forceinline__ int acc_row(int wm, int mb, int i, int lane) {
-  return wm * C::WTM + mb * 32 + (i >> 2) * 8 + (lane >> 5) * 4 + (i & 3);
+// Accumulator layout.  The MFMA is given the B fragment as its first operand,
+// so block (mb, nb) holds the transposed product: element q of a lane sits at
+// tile row acc_row(wm, mb, lane) and tile column acc_col(wn, nb, q / 4, lane)
+// + q % 4.  Each lane thus owns one output row and four runs of four
+// consecutive columns per block, which the epilogues move with 8- or 16-byte
+// accesses.
+template <class C> __device__ __forceinline__ int acc_row(int wm, int mb, int lane) {
+  return wm * C::WTM + mb * 32 + (lane & 31);
 }
-template <class C> __device__ __forceinline__ int acc_col(int wn, int nb, int lane) {
-  return wn * C::WTN + nb * 32 + (lane & 31);
+template <class C> __device__ __forceinline__ int acc_col(int wn, int nb, int gq, int lane) {
+  return wn * C::WTN + nb * 32 + gq * 8 + (lane >> 5) * 4;
+}
+// the four values of run gq of block acc
+__device__ __forceinline__ void acc_run(const f32x16_t& acc, int gq, float (&f)[4]) {
+#pragma clang loop unroll(full)
+  for (int c = 0; c < 4; ++c) f[c] = acc[gq * 4 + c];
 }
 
 struct Tile {
@@ -353,17 +363,46 @@ template <typename T> __device__ __forceinline__ const char* cptr(const void* ba
   return (const char*)base + el * (int64_t)sizeof(T);
 }
 
+// Plain epilogue of a row-grouped problem: out[m0 + r, n0 + c] = acc, for
+// an output of `ld` columns (ld % 64 == 0).
+template <typename T, class C>
+__device__ __forceinline__ void store_rows(const Accum<C>& acc, T* out, int ld, const Tile& t, int wm,
+                                           int wn, int lane) {
+#pragma clang loop unroll(full)
+  for (int mb = 0; mb < C::MB; ++mb) {
+    const int r = acc_row<C>(wm, mb, lane);
+    if (r >= t.mrows) continue;
+    T* o = out + (int64_t)(t.m0 + r) * ld;
+#pragma clang loop unroll(full)
+    for (int nb = 0; nb < C::NB; ++nb)
+#pragma clang loop unroll(full)
+      for (int gq = 0; gq < 4; ++gq) {
+        const int n = t.n0 + acc_col<C>(wn, nb, gq, lane);
+        if (n >= ld) continue;
+        float v[4];
+        acc_run(acc.v[mb][nb], gq, v);
+        Vec4<T>::store(o + n, v);
+      }
+  }
+}
+
 // ================================================================ problems
 // Each problem provides locate (tile of this workgroup), init (buffer
 // resources and per-lane copy offsets), issue (start the direct copies of one
 // K tile into LDS), and epilogue (consume the accumulators).
 
-// Forward FC1 + SwiGLU (and the backward's recompute of it).
+// FC1 + SwiGLU, forward and the backward's recomputation of it.
 //   A(m, kk) = X[tok(m0 + m), kk]            K = h  (gathered rows)
 //   B(nr, kk) = W1[e, wrow(nr), kk]          each wave's WTN tile columns are
 //   WTN/2 gate rows f followed by the WTN/2 up rows F + f of the same f, so
 //   every lane holds both halves of its SwiGLU pairs (blocks nb, nb + NB/2).
-template <typename T, class C, bool kRecompute> struct ProbFC1 {
+// Forward epilogue: a = silu(u_g) u_u.  Backward epilogue (kBwd; dA = dY W2
+// of the row is already in `ag`): with g the slot's gate and da = g dA,
+//   du_g = da u_u silu'(u_g),  du_u = da silu(u_g)   -> u  [n, 2F]
+//   g a                                              -> ag [n, F] (over dA)
+//   dgp[m, f / 32] = sum over 32 columns f of dA a    (gate-gradient partials)
+// Each dA element is read and then overwritten by the one lane that owns it.
+template <typename T, class C, bool kBwd> struct ProbFC1 {
   static constexpr int kHalf = C::WTN / 2;
   typedef KcOp<T, C::BM, C::NW, C::KB> OA;
   typedef KcOp<T, C::BN, C::NW, C::KB> OB;
@@ -372,10 +411,10 @@ template <typename T, class C, bool kRecompute> struct ProbFC1 {
   static int grid(const GemmArgs& g) {
     return row_tiles_bound(g.n, g.E, C::BM) * ((g.F + C::BN / 2 - 1) / (C::BN / 2));
   }
-  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t) const {
+  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t, int id, int n) const {
     const int ntn = (g.F + C::BN / 2 - 1) / (C::BN / 2);
     int mt, nt;
-    tile_coords(g.raster, blockIdx.x, gridDim.x, gridDim.x / ntn, ntn, mt, nt);
+    tile_coords(g.raster, id, n, n / ntn, ntn, mt, nt);
     if (!locate_rows<C::BM>(g.offsets, g.E, mt, t)) return false;
     t.n0 = nt * (C::BN / 2);
     t.K = g.h;
@@ -401,28 +440,97 @@ template <typename T, class C, bool kRecompute> struct ProbFC1 {
   }
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
                                            int wm, int wn, int lane) const {
+    if constexpr (kBwd) {
+      epilogue_bwd(g, t, acc, wm, wn, lane);
+    } else {
 #pragma clang loop unroll(full)
-    for (int nb = 0; nb < C::NB / 2; ++nb) {
-      const int f = t.n0 + wn * kHalf + nb * 32 + (lane & 31);
-      if (f >= g.F) continue;
+      for (int mb = 0; mb < C::MB; ++mb) {
+        const int r = acc_row<C>(wm, mb, lane);
+        if (r >= t.mrows) continue;
+        T* a = (T*)g.a + (t.m0 + r) * (int64_t)g.F;
 #pragma clang loop unroll(full)
-      for (int mb = 0; mb < C::MB; ++mb)
+        for (int nb = 0; nb < C::NB / 2; ++nb)
 #pragma clang loop unroll(full)
-        for (int i = 0; i < 16; ++i) {
-          const int r = acc_row<C>(wm, mb, i, lane);
-          if (r >= t.mrows) continue;
-          const int64_t row = t.m0 + r;
-          const float gate = acc.v[mb][nb][i], up = acc.v[mb][nb + C::NB / 2][i];
-          const float act = gate * sigmoidf_(gate) * up;
-          if (!kRecompute) {
-            Elem<T>::store((T*)g.a + row * g.F + f, act);
-          } else {
-            T* u = (T*)g.u + row * 2 * g.F;
-            Elem<T>::store(u + f, gate);
-            Elem<T>::store(u + g.F + f, up);
-            Elem<T>::store((T*)g.ag + row * g.F + f, g.gate_of_row[row] * act);
+          for (int gq = 0; gq < 4; ++gq) {
+            // F % 64 == 0: a run of 4 columns is entirely inside or outside
+            const int f = t.n0 + wn * kHalf + nb * 32 + gq * 8 + (lane >> 5) * 4;
+            if (f >= g.F) continue;
+            float gate[4], up[4], act[4];
+            acc_run(acc.v[mb][nb], gq, gate);
+            acc_run(acc.v[mb][nb + C::NB / 2], gq, up);
+#pragma clang loop unroll(full)
+            for (int c = 0; c < 4; ++c) act[c] = gate[c] * sigmoidf_(gate[c]) * up[c];
+            Vec4<T>::store(a + f, act);
+          }
+      }
+    }
+  }
+  // Steps walk the row blocks mb; the dA values of block mb + 1 are loaded
+  // while block mb is computed and stored (two buffers).  Rows past the tile
+  // and column blocks past F load from clamped in-range addresses and are not
+  // used.
+  __device__ __forceinline__ void epilogue_bwd(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
+                                               int wm, int wn, int lane) const {
+    typedef typename Vec4<T>::Raw Raw;
+    constexpr int NH = C::NB / 2;  // gate (and up) blocks per wave
+    Raw dar[2][NH][4];
+    float gtb[2];
+    auto fetch = [&](int mb, int b) {
+      const int r = acc_row<C>(wm, mb, lane);
+      const int64_t row = t.m0 + (r < t.mrows ? r : 0);
+      gtb[b] = g.gate_of_row[row];
+      const T* d = (const T*)g.ag + row * g.F;
+#pragma clang loop unroll(full)
+      for (int nb = 0; nb < NH; ++nb)
+#pragma clang loop unroll(full)
+        for (int gq = 0; gq < 4; ++gq) {
+          const int f = t.n0 + wn * kHalf + nb * 32 + gq * 8 + (lane >> 5) * 4;
+          dar[b][nb][gq] = Vec4<T>::load_raw(d + (f < g.F ? f : 0));
+        }
+    };
+    fetch(0, 0);
+#pragma clang loop unroll(full)
+    for (int mb = 0; mb < C::MB; ++mb) {
+      const int b = mb & 1;
+      if (mb + 1 < C::MB) fetch(mb + 1, b ^ 1);
+      const int r = acc_row<C>(wm, mb, lane);
+      const bool in = r < t.mrows;
+      const int64_t row = t.m0 + (in ? r : 0);
+      const float gt = gtb[b];
+      T* u = (T*)g.u + row * 2 * g.F;
+      T* ag = (T*)g.ag + row * g.F;
+#pragma clang loop unroll(full)
+      for (int nb = 0; nb < NH; ++nb) {
+        // F % 64 == 0 and the block starts at a multiple of 32: all or nothing
+        const int fb = t.n0 + wn * kHalf + nb * 32;
+        if (fb >= g.F) continue;
+        float part = 0.f;
+#pragma clang loop unroll(full)
+        for (int gq = 0; gq < 4; ++gq) {
+          float dA[4], gate[4], up[4], dug[4], duu[4], ga[4];
+          Vec4<T>::unpack(dar[b][nb][gq], dA);
+          acc_run(acc.v[mb][nb], gq, gate);
+          acc_run(acc.v[mb][nb + NH], gq, up);
+#pragma clang loop unroll(full)
+          for (int c = 0; c < 4; ++c) {
+            const float x = gate[c], s = sigmoidf_(x), silu = x * s, act = silu * up[c];
+            part = fmaf(dA[c], act, part);
+            const float da = gt * dA[c];
+            dug[c] = da * up[c] * s * (1.f + x * (1.f - s));
+            duu[c] = da * silu;
+            ga[c] = gt * act;
+          }
+          if (in) {
+            const int f = fb + gq * 8 + (lane >> 5) * 4;
+            Vec4<T>::store(u + f, dug);
+            Vec4<T>::store(u + g.F + f, duu);
+            Vec4<T>::store(ag + f, ga);
           }
         }
+        // the row's 32 columns of the block are split between lanes l and l + 32
+        part += __shfl_xor(part, 32, 64);
+        if (in && lane < 32) g.dgp[row * g.P + fb / 32] = part;
+      }
     }
   }
 };
@@ -436,10 +544,10 @@ template <typename T, class C> struct ProbFC2 {
   static int grid(const GemmArgs& g) {
     return row_tiles_bound(g.n, g.E, C::BM) * ((g.h + C::BN - 1) / C::BN);
   }
-  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t) const {
+  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t, int id, int n) const {
     const int ntn = (g.h + C::BN - 1) / C::BN;
     int mt, nt;
-    tile_coords(g.raster, blockIdx.x, gridDim.x, gridDim.x / ntn, ntn, mt, nt);
+    tile_coords(g.raster, id, n, n / ntn, ntn, mt, nt);
     if (!locate_rows<C::BM>(g.offsets, g.E, mt, t)) return false;
     t.n0 = nt * C::BN;
     t.K = g.F;
@@ -459,27 +567,12 @@ template <typename T, class C> struct ProbFC2 {
   }
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
                                            int wm, int wn, int lane) const {
-#pragma clang loop unroll(full)
-    for (int nb = 0; nb < C::NB; ++nb) {
-      const int n = t.n0 + acc_col<C>(wn, nb, lane);
-      if (n >= g.h) continue;
-#pragma clang loop unroll(full)
-      for (int mb = 0; mb < C::MB; ++mb)
-#pragma clang loop unroll(full)
-        for (int i = 0; i < 16; ++i) {
-          const int r = acc_row<C>(wm, mb, i, lane);
-          if (r < t.mrows) Elem<T>::store((T*)g.y + (int64_t)(t.m0 + r) * g.h + n, acc.v[mb][nb][i]);
-        }
-    }
+    store_rows<T, C>(acc, (T*)g.y, g.h, t, wm, wn, lane);
   }
 };
 
-// Backward FC2 dgrad with the SwiGLU backward and the gate-gradient partial
-// fused into the epilogue:
-//   dA[m, f] = sum_o dY[tok(m), o] W2[e, o, f]          K = h
-//   a = silu(u_g) u_u;  da = g dA;  du_g = da u_u silu'(u_g);  du_u = da silu(u_g)
-//   dgp[m, f / 64] = sum over the 64 columns f of one pair of blocks of dA * a
-// du overwrites u in place (each element is read and written by one lane).
+// Backward FC2 dgrad: dA[m, f] = sum_o dY[tok(m), o] W2[e, o, f]     K = h
+// (written to `ag`; the SwiGLU backward happens in the FC1 recomputation).
 template <typename T, class C> struct ProbFC2Dgrad {
   typedef KcOp<T, C::BM, C::NW, C::KB> OA;
   typedef KsOp<T, C::BN, C::NW, C::KB> OB;
@@ -489,15 +582,16 @@ template <typename T, class C> struct ProbFC2Dgrad {
   static int grid(const GemmArgs& g) {
     return row_tiles_bound(g.n, g.E, C::BM) * ((g.F + C::BN - 1) / C::BN);
   }
-  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t) const {
+  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t, int id, int n) const {
     const int ntn = (g.F + C::BN - 1) / C::BN;
     int mt, nt;
-    tile_coords(g.raster, blockIdx.x, gridDim.x, gridDim.x / ntn, ntn, mt, nt);
+    tile_coords(g.raster, id, n, n / ntn, ntn, mt, nt);
     if (!locate_rows<C::BM>(g.offsets, g.E, mt, t)) return false;
     t.n0 = nt * C::BN;
     t.K = g.h;
     return true;
   }
+  __device__ __forceinline__ static int reduction(const GemmArgs& g) { return g.h; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
     A.rs = make_rsrc(g.dY, g.T_h_bytes);
     const int32_t* tok = g.tok_of_row + t.m0;
@@ -519,61 +613,7 @@ template <typename T, class C> struct ProbFC2Dgrad {
   }
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
                                            int wm, int wn, int lane) const {
-#pragma clang loop unroll(full)
-    for (int pb = 0; pb < C::NB / 2; ++pb) {  // pairs of 32-column blocks
-      const int f0 = t.n0 + acc_col<C>(wn, 2 * pb, 0);
-#pragma clang loop unroll(full)
-      for (int mb = 0; mb < C::MB; ++mb) {
-        float part[16];
-#pragma clang loop unroll(full)
-        for (int i = 0; i < 16; ++i) part[i] = 0.f;
-#pragma clang loop unroll(full)
-        for (int h2 = 0; h2 < 2; ++h2) {
-          const int nb = 2 * pb + h2;
-          const int f = t.n0 + acc_col<C>(wn, nb, lane);
-          if (f >= g.F) continue;
-          // read the block's u values first, then compute and write du
-          float ug[16], uu[16], gt[16];
-#pragma clang loop unroll(full)
-          for (int i = 0; i < 16; ++i) {
-            const int r = acc_row<C>(wm, mb, i, lane);
-            const bool in = r < t.mrows;
-            const int64_t row = t.m0 + (in ? r : 0);
-            const T* u = (const T*)g.u + row * 2 * g.F;
-            // unconditional loads (row is clamped into the tile): no branch
-            // splits the batch
-            const float vg = Elem<T>::load(u + f), vu = Elem<T>::load(u + g.F + f);
-            const float vt = g.gate_of_row[row];
-            ug[i] = in ? vg : 0.f;
-            uu[i] = in ? vu : 0.f;
-            gt[i] = in ? vt : 0.f;
-          }
-#pragma clang loop unroll(full)
-          for (int i = 0; i < 16; ++i) {
-            const int r = acc_row<C>(wm, mb, i, lane);
-            const float s = sigmoidf_(ug[i]), silu = ug[i] * s;
-            const float dA = acc.v[mb][nb][i];
-            part[i] = fmaf(dA, silu * uu[i], part[i]);
-            const float da = gt[i] * dA;
-            if (r < t.mrows) {
-              T* u = (T*)g.u + (int64_t)(t.m0 + r) * 2 * g.F;
-              Elem<T>::store(u + f, da * uu[i] * s * (1.f + ug[i] * (1.f - s)));
-              Elem<T>::store(u + g.F + f, da * silu);
-            }
-          }
-        }
-        // sum over the 32 columns held by the lanes with equal lane >> 5
-#pragma clang loop unroll(full)
-        for (int i = 0; i < 16; ++i) {
-          float v = part[i];
-#pragma clang loop unroll(full)
-          for (int o = 1; o < 32; o <<= 1) v += __shfl_xor(v, o, 64);
-          const int r = acc_row<C>(wm, mb, i, lane);
-          if ((lane & 31) == 0 && r < t.mrows && f0 < g.F)
-            g.dgp[(int64_t)(t.m0 + r) * g.P + f0 / 64] = v;
-        }
-      }
-    }
+    store_rows<T, C>(acc, (T*)g.ag, g.F, t, wm, wn, lane);
   }
 };
 
@@ -587,15 +627,16 @@ template <typename T, class C> struct ProbFC1Dgrad {
   static int grid(const GemmArgs& g) {
     return row_tiles_bound(g.n, g.E, C::BM) * ((g.h + C::BN - 1) / C::BN);
   }
-  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t) const {
+  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t, int id, int n) const {
     const int ntn = (g.h + C::BN - 1) / C::BN;
     int mt, nt;
-    tile_coords(g.raster, blockIdx.x, gridDim.x, gridDim.x / ntn, ntn, mt, nt);
+    tile_coords(g.raster, id, n, n / ntn, ntn, mt, nt);
     if (!locate_rows<C::BM>(g.offsets, g.E, mt, t)) return false;
     t.n0 = nt * C::BN;
     t.K = 2 * g.F;
     return true;
   }
+  __device__ __forceinline__ static int reduction(const GemmArgs& g) { return 2 * g.F; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
     const uint32_t rowb = (uint32_t)2 * g.F * sizeof(T);
     A.rs = make_rsrc(cptr<T>(g.u, (int64_t)t.m0 * 2 * g.F), (int64_t)t.mrows * rowb);
@@ -616,18 +657,7 @@ template <typename T, class C> struct ProbFC1Dgrad {
   }
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
                                            int wm, int wn, int lane) const {
-#pragma clang loop unroll(full)
-    for (int nb = 0; nb < C::NB; ++nb) {
-      const int n = t.n0 + acc_col<C>(wn, nb, lane);
-      if (n >= g.h) continue;
-#pragma clang loop unroll(full)
-      for (int mb = 0; mb < C::MB; ++mb)
-#pragma clang loop unroll(full)
-        for (int i = 0; i < 16; ++i) {
-          const int r = acc_row<C>(wm, mb, i, lane);
-          if (r < t.mrows) Elem<T>::store((T*)g.dxp + (int64_t)(t.m0 + r) * g.h + n, acc.v[mb][nb][i]);
-        }
-    }
+    store_rows<T, C>(acc, (T*)g.dxp, g.h, t, wm, wn, lane);
   }
 };
 
@@ -649,16 +679,17 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
   int32_t tok[D][IG];        // gathered operand: tokens of the next D K tiles' rows
   __host__ __device__ static int M(const GemmArgs& g) { return kFC1 ? 2 * g.F : g.h; }
   __host__ __device__ static int N(const GemmArgs& g) { return kFC1 ? g.h : g.F; }
-  static int grid(const GemmArgs& g) {
-    return g.E * ((M(g) + C::BM - 1) / C::BM) * ((N(g) + C::BN - 1) / C::BN);
+  __host__ __device__ static int tiles_per_expert(const GemmArgs& g) {
+    return ((M(g) + C::BM - 1) / C::BM) * ((N(g) + C::BN - 1) / C::BN);
   }
-  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t) const {
+  static int grid(const GemmArgs& g) { return g.E * tiles_per_expert(g); }
+  __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t, int id, int n) const {
     const int mtn = (M(g) + C::BM - 1) / C::BM, ntn = (N(g) + C::BN - 1) / C::BN;
     const int per = mtn * ntn;
     // experts in descending row count; within an expert, XCD-grouped tiles
-    const int rank = blockIdx.x / per;
+    const int rank = id / per;
     int mt, nt;
-    tile_coords(g.raster, blockIdx.x - rank * per, per, mtn, ntn, mt, nt);
+    tile_coords(g.raster, id - rank * per, per, mtn, ntn, mt, nt);
     t.e = g.order[rank];
     t.r0 = g.offsets[t.e];
     t.K = g.offsets[t.e + 1] - t.r0;
@@ -743,29 +774,44 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
                                            int wm, int wn, int lane) const {
     float* dW = (kFC1 ? g.dW1 : g.dW2) + (int64_t)t.e * M(g) * N(g);
-    const int Nn = N(g);
-    // all loads of a block before its stores: the old values are read in one
-    // batch instead of one load-add-store round trip per element
+    const int Nn = N(g);  // % 64 == 0: a run of 4 columns is all in or all out
+    // Accumulating: the old values of row block mb + 1 are loaded while block
+    // mb is added and stored (two buffers).  Rows past the tile and runs past
+    // N load from clamped in-range addresses and are not used.
+    typedef Vec4<float>::Raw Raw;
+    constexpr int NR = C::NB * 4;
+    Raw old[2][NR];
+    auto fetch = [&](int mb, int b) {
+      const int r = acc_row<C>(wm, mb, lane);
+      const float* o = dW + (int64_t)(t.m0 + (r < t.mrows ? r : 0)) * Nn;
 #pragma clang loop unroll(full)
-    for (int nb = 0; nb < C::NB; ++nb) {
-      const int n = t.n0 + acc_col<C>(wn, nb, lane);
-      const bool nin = n < Nn;
+      for (int nb = 0; nb < C::NB; ++nb)
 #pragma clang loop unroll(full)
-      for (int mb = 0; mb < C::MB; ++mb) {
-        float old[16];
-#pragma clang loop unroll(full)
-        for (int i = 0; i < 16; ++i) {
-          const int r = acc_row<C>(wm, mb, i, lane);
-          const bool in = nin && r < t.mrows;
-          const float v = g.accumulate ? dW[(int64_t)(t.m0 + (in ? r : 0)) * Nn + (in ? n : t.n0)] : 0.f;
-          old[i] = in ? v : 0.f;
+        for (int gq = 0; gq < 4; ++gq) {
+          const int n = t.n0 + acc_col<C>(wn, nb, gq, lane);
+          old[b][nb * 4 + gq] = Vec4<float>::load_raw(o + (n < Nn ? n : t.n0));
         }
+    };
+    if (g.accumulate) fetch(0, 0);
 #pragma clang loop unroll(full)
-        for (int i = 0; i < 16; ++i) {
-          const int r = acc_row<C>(wm, mb, i, lane);
-          if (nin && r < t.mrows) dW[(int64_t)(t.m0 + r) * Nn + n] = old[i] + acc.v[mb][nb][i];
+    for (int mb = 0; mb < C::MB; ++mb) {
+      const int b = mb & 1;
+      if (g.accumulate && mb + 1 < C::MB) fetch(mb + 1, b ^ 1);
+      const int r = acc_row<C>(wm, mb, lane);
+      if (r >= t.mrows) continue;
+      float* o = dW + (int64_t)(t.m0 + r) * Nn;
+#pragma clang loop unroll(full)
+      for (int nb = 0; nb < C::NB; ++nb)
+#pragma clang loop unroll(full)
+        for (int gq = 0; gq < 4; ++gq) {
+          const int n = t.n0 + acc_col<C>(wn, nb, gq, lane);
+          if (n >= Nn) continue;
+          float v[4] = {0.f, 0.f, 0.f, 0.f};
+          if (g.accumulate) Vec4<float>::unpack(old[b][nb * 4 + gq], v);
+#pragma clang loop unroll(full)
+          for (int c = 0; c < 4; ++c) v[c] += acc.v[mb][nb][gq * 4 + c];
+          Vec4<float>::store(o + n, v);
         }
-      }
     }
   }
 };
@@ -784,12 +830,10 @@ template <int N> __device__ __forceinline__ void wait_vm() {
 // publishes every wave's copies and also certifies that all waves are done
 // with tile kt-1, whose stage the next copy overwrites.
 template <typename T, class C, class P>
-__global__ __launch_bounds__(C::kThreads, C::kMinWaves)
-__attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_gemm_kernel(GemmArgs g) {
-  __shared__ __attribute__((aligned(1024))) char smem[C::kLds];
+__device__ __forceinline__ void run_tile(const GemmArgs& g, char* smem, int id, int n) {
   P p;
   Tile t;
-  if (!p.locate(g, t)) return;
+  if (!p.locate(g, t, id, n)) return;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w / C::WN, wn = w % C::WN;
   p.init(g, t, w, lane);
   Accum<C> acc;
@@ -821,6 +865,49 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
   p.epilogue(g, t, acc, wm, wn, lane);
 }
 
+template <typename T, class C, class P>
+__global__ __launch_bounds__(C::kThreads, C::kMinWaves)
+__attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_gemm_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(1024))) char smem[C::kLds];
+  run_tile<T, C, P>(g, smem, blockIdx.x, gridDim.x);
+}
+
+// The dgrad and the wgrad of one FC layer in one launch (nd + nw workgroups;
+// the two problems are independent).  Every dgrad tile reduces over the same
+// K (h or 2F); a wgrad tile reduces over its expert's rows.  Workgroups are
+// dealt longest tile first, as far as that matters: first the wgrad tiles of
+// the experts with at least K rows (the wgrad grid already lists experts by
+// descending rows), then the dgrad tiles and the remaining, shorter wgrad
+// tiles interleaved in proportion (workgroup j of this part runs dgrad tile
+// floor(j nd / m) when that value steps at j, else the next wgrad tile).  The
+// CUs thus run a mix of both problems: the memory-heavy epilogues of one
+// overlap the matrix-core phases of the other, and neither leaves a
+// half-empty last round.
+template <typename T, class C, class PD, class PW>
+__global__ __launch_bounds__(C::kThreads, C::kMinWaves)
+__attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_gemm_bwd_pair_kernel(
+    GemmArgs g, int nd, int nw) {
+  __shared__ __attribute__((aligned(1024))) char smem[C::kLds];
+  const int Kd = PD::reduction(g);
+  // first rank (experts by descending rows) with fewer than Kd rows
+  int lo = 0, hi = g.E;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1, e = g.order[mid];
+    if (g.offsets[e + 1] - g.offsets[e] >= Kd) lo = mid + 1;
+    else hi = mid;
+  }
+  const int lead = lo * PW::tiles_per_expert(g);
+  const int i = blockIdx.x;
+  if (i < lead) {
+    run_tile<T, C, PW>(g, smem, i, nw);
+    return;
+  }
+  const int64_t j = i - lead, m = (int64_t)nd + (nw - lead);
+  const int a = (int)(j * nd / m), b = (int)((j + 1) * nd / m);
+  if (b > a) run_tile<T, C, PD>(g, smem, a, nd);
+  else run_tile<T, C, PW>(g, smem, lead + (int)(j - a), nw);
+}
+
 template <template <typename, class> class PT, class C>
 hipError_t launch_cfg(const GemmArgs& g, hipStream_t s) {
   const int blocks = PT<float, C>::grid(g);
@@ -830,6 +917,22 @@ hipError_t launch_cfg(const GemmArgs& g, hipStream_t s) {
   else
     grouped_gemm_kernel<float, Small, PT<float, Small>><<<PT<float, Small>::grid(g), Small::kThreads,
                                                           0, s>>>(g);
+  return hipGetLastError();
+}
+
+template <template <typename, class> class P1, template <typename, class> class P2, class C>
+hipError_t launch_pair_cfg(const GemmArgs& g, hipStream_t s) {
+  if (g.dtype != 0) {
+    const int n1 = P1<float, Small>::grid(g), n2 = P2<float, Small>::grid(g);
+    if (n1 + n2 <= 0) return hipSuccess;
+    grouped_gemm_bwd_pair_kernel<float, Small, P1<float, Small>, P2<float, Small>>
+        <<<n1 + n2, Small::kThreads, 0, s>>>(g, n1, n2);
+  } else {
+    const int n1 = P1<bf16_t, C>::grid(g), n2 = P2<bf16_t, C>::grid(g);
+    if (n1 + n2 <= 0) return hipSuccess;
+    grouped_gemm_bwd_pair_kernel<bf16_t, C, P1<bf16_t, C>, P2<bf16_t, C>>
+        <<<n1 + n2, C::kThreads, 0, s>>>(g, n1, n2);
+  }
   return hipGetLastError();
 }
 
@@ -866,21 +969,31 @@ hipError_t launch_auto(const GemmArgs& g, hipStream_t s) {
   return launch_cfg<PT, Small>(g, s);
 }
 
+template <template <typename, class> class P1, template <typename, class> class P2>
+hipError_t launch_pair(const GemmArgs& g, hipStream_t s) {
+  if (g.dtype == 0 && P1<float, Big8>::grid(g) + P2<float, Big8>::grid(g) < 128)
+    return launch_pair_cfg<P1, P2, Small>(g, s);
+  return launch_pair_cfg<P1, P2, Big8>(g, s);
+}
+
 template <typename T, class C> using FC1Fwd = ProbFC1<T, C, false>;
-template <typename T, class C> using FC1Rec = ProbFC1<T, C, true>;
+template <typename T, class C> using FC1Bwd = ProbFC1<T, C, true>;
 template <typename T, class C> using FC2W = ProbWgrad<T, C, false>;
 template <typename T, class C> using FC1W = ProbWgrad<T, C, true>;
 
 }  // namespace
 
-int dgate_partials(int F) { return (F + 63) / 64; }
+int dgate_partials(int F) { return (F + 31) / 32; }
 
 hipError_t launch_fc1_fwd(const GemmArgs& g, hipStream_t s) { return launch_auto<FC1Fwd>(g, s); }
-hipError_t launch_fc1_recompute(const GemmArgs& g, hipStream_t s) { return launch_auto<FC1Rec>(g, s); }
+hipError_t launch_fc1_recompute(const GemmArgs& g, hipStream_t s) { return launch_auto<FC1Bwd>(g, s); }
 hipError_t launch_fc2_fwd(const GemmArgs& g, hipStream_t s) { return launch_auto<ProbFC2>(g, s); }
 hipError_t launch_fc2_dgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<ProbFC2Dgrad>(g, s); }
 hipError_t launch_fc1_dgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<ProbFC1Dgrad>(g, s); }
 hipError_t launch_fc2_wgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<FC2W>(g, s); }
 hipError_t launch_fc1_wgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<FC1W>(g, s); }
+hipError_t launch_fc1_dgrad_wgrad(const GemmArgs& g, hipStream_t s) {
+  return launch_pair<ProbFC1Dgrad, FC1W>(g, s);
+}
 
 }  // namespace memfine

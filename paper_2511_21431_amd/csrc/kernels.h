@@ -55,8 +55,8 @@ struct GemmArgs {
   const void* W2;    // [E, h, F]
   void* a;           // [n, F]   forward SwiGLU output
   void* y;           // [n, h]   forward expert output
-  void* u;           // [n, 2F]  backward: FC1 recompute output, then du in place
-  void* ag;          // [n, F]   backward: gate * SwiGLU output
+  void* u;           // [n, 2F]  backward: du
+  void* ag;          // [n, F]   backward: dA, then gate * SwiGLU output in place
   void* dxp;         // [n, h]   backward: input gradient per row
   float* dgp;        // [n, P]   backward: partial gate gradients
   int P;             // partials per row
@@ -77,5 +77,7 @@ hipError_t launch_fc2_dgrad(const GemmArgs& g, hipStream_t s);
 hipError_t launch_fc2_wgrad(const GemmArgs& g, hipStream_t s);
 hipError_t launch_fc1_wgrad(const GemmArgs& g, hipStream_t s);
 hipError_t launch_fc1_dgrad(const GemmArgs& g, hipStream_t s);
+// FC1 dgrad and FC1 wgrad in one launch (independent problems).
+hipError_t launch_fc1_dgrad_wgrad(const GemmArgs& g, hipStream_t s);
 
 }  // namespace memfine

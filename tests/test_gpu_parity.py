@@ -223,6 +223,31 @@ def test_degenerate_cases(mf):
     assert float(dW1.abs().max()) == 0.0 and float(dW2.abs().max()) == 0.0
 
 
+def test_out_of_range_ids_are_dropped(mf):
+    """A slot whose id lies outside [0, E) contributes nothing.  Reference: the
+    oracle with that slot sent to expert 0 at gate 0 (a zero gate removes the
+    slot from Y, dX and dW), and dgates 0 at the dropped slots."""
+    w, case = small_case("cfg2-like")
+    bad = case["idx"].copy()
+    rng = np.random.default_rng(7)
+    drop = rng.random(bad.shape) < 0.1
+    bad[drop] = np.where(rng.random(drop.sum()) < 0.5, -1, w.E + 5).astype(np.int32)
+    ref_idx = np.where(drop, 0, case["idx"]).astype(np.int32)
+    ref_g = np.where(drop, 0.0, case["gates"]).astype(np.float32)
+    dev = device_case(w, dict(case, idx=bad))
+    for C in (1, 3):
+        log(f"dropped ids C={C}")
+        Y = host(run_fwd(w, dev, C))
+        B = run_bwd(w, dev, C)
+        Y_ref = om.moe_fwd(case["X"], ref_idx, ref_g, case["W1"], case["W2"], C)
+        R = om.moe_bwd(case["X"], ref_idx, ref_g, case["W1"], case["W2"], case["dY"], C)
+        R["dgates"] = np.where(drop, 0.0, R["dgates"])
+        assert relerr(Y, Y_ref) <= TOL[w.dtype]
+        for key in ("dX", "dgates", "dW1", "dW2"):
+            assert relerr(host(B[key]), R[key]) <= TOL[w.dtype], key
+        assert np.all(host(B["dgates"])[drop] == 0.0)
+
+
 def test_allocator_hook_peak_and_oom(mf):
     """The working memory the layer holds at once, measured two ways (the
     allocator hook's own high-water mark, and torch's allocator statistics),
