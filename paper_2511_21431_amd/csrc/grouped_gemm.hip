@@ -56,9 +56,12 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
 
 // Tile shape: BM x BN output per workgroup of WM x WN waves, S LDS stages of
-// KB bytes of K per operand row.
-template <int BM_, int BN_, int WM_, int WN_, int S_, int KB_ = 128> struct Cfg {
+// KB bytes of K per operand row.  DIRECT: operand tiles go from HBM straight
+// into LDS (buffer_load ... lds); else through registers (buffer_load into
+// VGPRs during the multiply of the previous tile, then ds_write_b128).
+template <int BM_, int BN_, int WM_, int WN_, int S_, int KB_ = 128, int DIRECT_ = 1> struct Cfg {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, S = S_, KB = KB_;
+  static constexpr bool DIRECT = DIRECT_ != 0;
   static constexpr int NW = WM * WN, kThreads = 64 * NW;
   static constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
   static constexpr int MB = WTM / 32, NB = WTN / 32;  // 32x32 MFMA blocks per wave
@@ -113,6 +116,9 @@ __device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, char* lds, 
                                            uint32_t soff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds, 16, voff, soff, 0, 0);
 }
+__device__ __forceinline__ u32x4_t load_reg16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
 
 template <typename T> struct Mma;
 template <> struct Mma<bf16_t> {
@@ -155,7 +161,7 @@ __device__ __forceinline__ float kc_read_f32(const char* lds, int row0, int kk, 
   return *(const float*)(lds + kc_off<KB>(row, kel >> 2) + ((kel & 3) << 2));
 }
 
-template <typename T, int ROWS, int NW, int KB> struct KcOp {
+template <typename T, int ROWS, int NW, int KB, bool DIRECT> struct KcOp {
   static constexpr int kReadsPerFrag = 1;
   static constexpr int U = KB / 16;          // 16-byte units per row
   static constexpr int RPI = 1024 / KB;      // rows per copy instruction
@@ -163,6 +169,7 @@ template <typename T, int ROWS, int NW, int KB> struct KcOp {
   static_assert(I * RPI * NW == ROWS, "tile rows must split evenly over the waves");
   __amdgpu_buffer_rsrc_t rs;
   uint32_t voff[I];
+  u32x4_t stage[DIRECT ? 1 : I];  // register-staged copy of one K tile
   __device__ __forceinline__ static int row_of(int i, int wave, int lane) {
     return RPI * (i * NW + wave) + lane / U;
   }
@@ -175,9 +182,19 @@ template <typename T, int ROWS, int NW, int KB> struct KcOp {
       voff[i] = rb == kOOB ? kOOB : rb + (uint32_t)((((lane % U) ^ kc_sw<KB>(row)) << 4));
     }
   }
-  __device__ __forceinline__ void issue(char* lds, int kt, int wave) const {
+  __device__ __forceinline__ void issue(char* lds, int kt, int wave) {
 #pragma clang loop unroll(full)
-    for (int i = 0; i < I; ++i) load_lds16(rs, lds + (i * NW + wave) * 1024, voff[i], kt * KB);
+    for (int i = 0; i < I; ++i) {
+      if constexpr (DIRECT) load_lds16(rs, lds + (i * NW + wave) * 1024, voff[i], kt * KB);
+      else stage[i] = load_reg16(rs, voff[i], kt * KB);
+    }
+  }
+  // register-staged copy: write the K tile to LDS where the direct copy would
+  __device__ __forceinline__ void commit(char* lds, int wave, int lane) const {
+    if constexpr (!DIRECT) {
+#pragma clang loop unroll(full)
+      for (int i = 0; i < I; ++i) *(u32x4_t*)(lds + (i * NW + wave) * 1024 + lane * 16) = stage[i];
+    }
   }
   __device__ __forceinline__ static typename Mma<T>::Frag read(const char* lds, int row0, int kk,
                                                                int lane) {
@@ -196,7 +213,7 @@ __device__ __forceinline__ int ks_sw(int k) {
   return ((k & 1) * 10) ^ ((k & 2) * 2);
 }
 
-template <typename T, int ROWS, int NW, int KB> struct KsOp {
+template <typename T, int ROWS, int NW, int KB, bool DIRECT> struct KsOp {
   static constexpr int kReadsPerFrag = sizeof(T) == 2 ? 2 : 1;
   static constexpr int BKE = KB / (int)sizeof(T);  // k-rows per K tile
   static constexpr int P = ROWS * (int)sizeof(T);
@@ -206,6 +223,7 @@ template <typename T, int ROWS, int NW, int KB> struct KsOp {
   static constexpr int V = 16 / (int)sizeof(T); // elements per 16-byte unit
   __amdgpu_buffer_rsrc_t rs;
   uint32_t voff[I];
+  u32x4_t stage[DIRECT ? 1 : I];  // register-staged copy of one K tile
   // lane's k-row (within the K tile) and logical element column of instruction i
   __device__ __forceinline__ static int k_of(int i, int wave, int lane) {
     return (i * NW + wave) * KPI + (lane * 16) / P;
@@ -215,9 +233,18 @@ template <typename T, int ROWS, int NW, int KB> struct KsOp {
     const int p = ((lane * 16) % P) >> 4;
     return (p ^ ks_sw(k)) * V;
   }
-  __device__ __forceinline__ void issue(char* lds, uint32_t soff, int wave) const {
+  __device__ __forceinline__ void issue(char* lds, uint32_t soff, int wave) {
 #pragma clang loop unroll(full)
-    for (int i = 0; i < I; ++i) load_lds16(rs, lds + (i * NW + wave) * 1024, voff[i], soff);
+    for (int i = 0; i < I; ++i) {
+      if constexpr (DIRECT) load_lds16(rs, lds + (i * NW + wave) * 1024, voff[i], soff);
+      else stage[i] = load_reg16(rs, voff[i], soff);
+    }
+  }
+  __device__ __forceinline__ void commit(char* lds, int wave, int lane) const {
+    if constexpr (!DIRECT) {
+#pragma clang loop unroll(full)
+      for (int i = 0; i < I; ++i) *(u32x4_t*)(lds + (i * NW + wave) * 1024 + lane * 16) = stage[i];
+    }
   }
   __device__ __forceinline__ static int phys(int k, int col) {  // byte of element col in k-row
     const int b = col * (int)sizeof(T);
@@ -251,8 +278,8 @@ template <int ROWS>
 __device__ __forceinline__ float ks_read_f32(const char* lds, int col0, int kk, int lane) {
   return *(const float*)(lds + ks_phys<ROWS * 4, 4>(kk * 2 + (lane >> 5), col0 + (lane & 31)));
 }
-template <typename T, int ROWS, int NW, int KB>
-__device__ __forceinline__ typename Mma<T>::Frag KsOp<T, ROWS, NW, KB>::read(const char* lds, int col0,
+template <typename T, int ROWS, int NW, int KB, bool DIRECT>
+__device__ __forceinline__ typename Mma<T>::Frag KsOp<T, ROWS, NW, KB, DIRECT>::read(const char* lds, int col0,
                                                                        int kk, int lane) {
   if constexpr (sizeof(T) == 2) return ks_read_bf16<ROWS>(lds, col0, kk, lane);
   else return ks_read_f32<ROWS>(lds, col0, kk, lane);
@@ -261,6 +288,14 @@ __device__ __forceinline__ typename Mma<T>::Frag KsOp<T, ROWS, NW, KB>::read(con
 template <class C> struct Accum {
   f32x16_t v[C::MB][C::NB];
 };
+template <class C> __device__ __forceinline__ void zero_acc(Accum<C>& acc) {
+#pragma clang loop unroll(full)
+  for (int i = 0; i < C::MB; ++i)
+#pragma clang loop unroll(full)
+    for (int j = 0; j < C::NB; ++j)
+#pragma clang loop unroll(full)
+      for (int q = 0; q < 16; ++q) acc.v[i][j][q] = 0.f;
+}
 
 // One K tile: the operand fragments of K step kk+1 are read from LDS while
 // the MFMAs of step kk run (two fragment register sets); scheduling
@@ -404,8 +439,8 @@ __device__ __forceinline__ void store_rows(const Accum<C>& acc, T* out, int ld, 
 // Each dA element is read and then overwritten by the one lane that owns it.
 template <typename T, class C, bool kBwd> struct ProbFC1 {
   static constexpr int kHalf = C::WTN / 2;
-  typedef KcOp<T, C::BM, C::NW, C::KB> OA;
-  typedef KcOp<T, C::BN, C::NW, C::KB> OB;
+  typedef KcOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
+  typedef KcOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
   OA A;
   OB B;
   static int grid(const GemmArgs& g) {
@@ -432,6 +467,14 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
       const int wrow = q >= kHalf ? g.F + f : f;
       return f < g.F ? (uint32_t)wrow * rowb : kOOB;
     }, wave, lane);
+  }
+  __device__ __forceinline__ void init_acc(const GemmArgs&, const Tile&, Accum<C>& acc, int, int,
+                                          int) const {
+    zero_acc(acc);
+  }
+  __device__ __forceinline__ void commit(char* As, char* Bs, int wave, int lane) const {
+    A.commit(As, wave, lane);
+    B.commit(Bs, wave, lane);
   }
   __device__ __forceinline__ void issue(const GemmArgs&, const Tile&, int kt, char* As, char* Bs,
                                         int wave, int) {
@@ -537,8 +580,8 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
 
 // Forward FC2: y[m, n] = sum_f a[m, f] W2[e, n, f].     K = F
 template <typename T, class C> struct ProbFC2 {
-  typedef KcOp<T, C::BM, C::NW, C::KB> OA;
-  typedef KcOp<T, C::BN, C::NW, C::KB> OB;
+  typedef KcOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
+  typedef KcOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
   OA A;
   OB B;
   static int grid(const GemmArgs& g) {
@@ -560,6 +603,14 @@ template <typename T, class C> struct ProbFC2 {
     B.rs = make_rsrc(cptr<T>(g.W2, (int64_t)t.e * g.h * g.F), (int64_t)g.h * rowb);
     B.init([&](int r) { return t.n0 + r < g.h ? (uint32_t)(t.n0 + r) * rowb : kOOB; }, wave, lane);
   }
+  __device__ __forceinline__ void init_acc(const GemmArgs&, const Tile&, Accum<C>& acc, int, int,
+                                          int) const {
+    zero_acc(acc);
+  }
+  __device__ __forceinline__ void commit(char* As, char* Bs, int wave, int lane) const {
+    A.commit(As, wave, lane);
+    B.commit(Bs, wave, lane);
+  }
   __device__ __forceinline__ void issue(const GemmArgs&, const Tile&, int kt, char* As, char* Bs,
                                         int wave, int) {
     A.issue(As, kt, wave);
@@ -574,8 +625,8 @@ template <typename T, class C> struct ProbFC2 {
 // Backward FC2 dgrad: dA[m, f] = sum_o dY[tok(m), o] W2[e, o, f]     K = h
 // (written to `ag`; the SwiGLU backward happens in the FC1 recomputation).
 template <typename T, class C> struct ProbFC2Dgrad {
-  typedef KcOp<T, C::BM, C::NW, C::KB> OA;
-  typedef KsOp<T, C::BN, C::NW, C::KB> OB;
+  typedef KcOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
+  typedef KsOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
   OA A;
   OB B;
   uint32_t b_ktile;  // bytes of W2 per K tile (BK rows)
@@ -606,6 +657,14 @@ template <typename T, class C> struct ProbFC2Dgrad {
     }
     b_ktile = ld * OB::BKE;
   }
+  __device__ __forceinline__ void init_acc(const GemmArgs&, const Tile&, Accum<C>& acc, int, int,
+                                          int) const {
+    zero_acc(acc);
+  }
+  __device__ __forceinline__ void commit(char* As, char* Bs, int wave, int lane) const {
+    A.commit(As, wave, lane);
+    B.commit(Bs, wave, lane);
+  }
   __device__ __forceinline__ void issue(const GemmArgs&, const Tile&, int kt, char* As, char* Bs,
                                         int wave, int) {
     A.issue(As, kt, wave);
@@ -619,8 +678,8 @@ template <typename T, class C> struct ProbFC2Dgrad {
 
 // Backward FC1 dgrad: dxp[m, n] = sum_c du[m, c] W1[e, c, n].    K = 2F
 template <typename T, class C> struct ProbFC1Dgrad {
-  typedef KcOp<T, C::BM, C::NW, C::KB> OA;
-  typedef KsOp<T, C::BN, C::NW, C::KB> OB;
+  typedef KcOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
+  typedef KsOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
   OA A;
   OB B;
   uint32_t b_ktile;
@@ -650,6 +709,14 @@ template <typename T, class C> struct ProbFC1Dgrad {
     }
     b_ktile = ld * OB::BKE;
   }
+  __device__ __forceinline__ void init_acc(const GemmArgs&, const Tile&, Accum<C>& acc, int, int,
+                                          int) const {
+    zero_acc(acc);
+  }
+  __device__ __forceinline__ void commit(char* As, char* Bs, int wave, int lane) const {
+    A.commit(As, wave, lane);
+    B.commit(Bs, wave, lane);
+  }
   __device__ __forceinline__ void issue(const GemmArgs&, const Tile&, int kt, char* As, char* Bs,
                                         int wave, int) {
     A.issue(As, kt, wave);
@@ -669,8 +736,8 @@ template <typename T, class C> struct ProbFC1Dgrad {
 // table, one tile ahead.  Tiles (rank, mt, nt) visit experts in descending
 // row count.
 template <typename T, class C, bool kFC1> struct ProbWgrad {
-  typedef KsOp<T, C::BM, C::NW, C::KB> OA;
-  typedef KsOp<T, C::BN, C::NW, C::KB> OB;
+  typedef KsOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
+  typedef KsOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
   static constexpr int IG = kFC1 ? OB::I : OA::I;  // copy instructions of the gathered operand
   OA A;
   OB B;
@@ -754,6 +821,37 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
 #pragma clang loop unroll(full)
     for (int d = 0; d < D; ++d) load_tokens(g, t, d, wave, lane, tok[d]);
   }
+  // Accumulating into dW: the accumulators start from the old dW values,
+  // loaded with the tile's first operand copies (their latency overlaps),
+  // so the epilogue only stores.  Rows past the tile and runs past N load
+  // from clamped in-range addresses; those accumulators are never stored.
+  __device__ __forceinline__ void init_acc(const GemmArgs& g, const Tile& t, Accum<C>& acc, int wm,
+                                          int wn, int lane) const {
+    if (!g.accumulate) {
+      zero_acc(acc);
+      return;
+    }
+    const float* dW = (kFC1 ? g.dW1 : g.dW2) + (int64_t)t.e * M(g) * N(g);
+    const int Nn = N(g);
+#pragma clang loop unroll(full)
+    for (int mb = 0; mb < C::MB; ++mb) {
+      const int r = acc_row<C>(wm, mb, lane);
+      const float* o = dW + (int64_t)(t.m0 + (r < t.mrows ? r : 0)) * Nn;
+#pragma clang loop unroll(full)
+      for (int nb = 0; nb < C::NB; ++nb)
+#pragma clang loop unroll(full)
+        for (int gq = 0; gq < 4; ++gq) {
+          const int n = t.n0 + acc_col<C>(wn, nb, gq, lane);
+          const f32x4_t v = Vec4<float>::load_raw(o + (n < Nn ? n : t.n0));
+#pragma clang loop unroll(full)
+          for (int c = 0; c < 4; ++c) acc.v[mb][nb][gq * 4 + c] = v[c];
+        }
+    }
+  }
+  __device__ __forceinline__ void commit(char* As, char* Bs, int wave, int lane) const {
+    A.commit(As, wave, lane);
+    B.commit(Bs, wave, lane);
+  }
   __device__ __forceinline__ void issue(const GemmArgs& g, const Tile& t, int kt, char* As,
                                         char* Bs, int wave, int lane) {
     const uint32_t rowb = (uint32_t)g.h * sizeof(T);
@@ -775,28 +873,8 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
                                            int wm, int wn, int lane) const {
     float* dW = (kFC1 ? g.dW1 : g.dW2) + (int64_t)t.e * M(g) * N(g);
     const int Nn = N(g);  // % 64 == 0: a run of 4 columns is all in or all out
-    // Accumulating: the old values of row block mb + 1 are loaded while block
-    // mb is added and stored (two buffers).  Rows past the tile and runs past
-    // N load from clamped in-range addresses and are not used.
-    typedef Vec4<float>::Raw Raw;
-    constexpr int NR = C::NB * 4;
-    Raw old[2][NR];
-    auto fetch = [&](int mb, int b) {
-      const int r = acc_row<C>(wm, mb, lane);
-      const float* o = dW + (int64_t)(t.m0 + (r < t.mrows ? r : 0)) * Nn;
-#pragma clang loop unroll(full)
-      for (int nb = 0; nb < C::NB; ++nb)
-#pragma clang loop unroll(full)
-        for (int gq = 0; gq < 4; ++gq) {
-          const int n = t.n0 + acc_col<C>(wn, nb, gq, lane);
-          old[b][nb * 4 + gq] = Vec4<float>::load_raw(o + (n < Nn ? n : t.n0));
-        }
-    };
-    if (g.accumulate) fetch(0, 0);
 #pragma clang loop unroll(full)
     for (int mb = 0; mb < C::MB; ++mb) {
-      const int b = mb & 1;
-      if (g.accumulate && mb + 1 < C::MB) fetch(mb + 1, b ^ 1);
       const int r = acc_row<C>(wm, mb, lane);
       if (r >= t.mrows) continue;
       float* o = dW + (int64_t)(t.m0 + r) * Nn;
@@ -806,10 +884,8 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
         for (int gq = 0; gq < 4; ++gq) {
           const int n = t.n0 + acc_col<C>(wn, nb, gq, lane);
           if (n >= Nn) continue;
-          float v[4] = {0.f, 0.f, 0.f, 0.f};
-          if (g.accumulate) Vec4<float>::unpack(old[b][nb * 4 + gq], v);
-#pragma clang loop unroll(full)
-          for (int c = 0; c < 4; ++c) v[c] += acc.v[mb][nb][gq * 4 + c];
+          float v[4];
+          acc_run(acc.v[mb][nb], gq, v);
           Vec4<float>::store(o + n, v);
         }
     }
@@ -837,30 +913,54 @@ __device__ __forceinline__ void run_tile(const GemmArgs& g, char* smem, int id, 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w / C::WN, wn = w % C::WN;
   p.init(g, t, w, lane);
   Accum<C> acc;
-#pragma clang loop unroll(full)
-  for (int i = 0; i < C::MB; ++i)
-#pragma clang loop unroll(full)
-    for (int j = 0; j < C::NB; ++j)
-#pragma clang loop unroll(full)
-      for (int q = 0; q < 16; ++q) acc.v[i][j][q] = 0.f;
+  p.init_acc(g, t, acc, wm, wn, lane);
   constexpr int kCopies = P::OA::I + P::OB::I;  // copy instructions per wave per K tile
   constexpr int BKE = C::KB / (int)sizeof(T);  // K per tile
   const int nk = (t.K + BKE - 1) / BKE;
+  if constexpr (C::DIRECT) {
 #pragma clang loop unroll(full)
-  for (int j = 0; j < C::S - 1; ++j) {
-    char* st = smem + j * C::kStage;
-    if (j < nk) p.issue(g, t, j, st, st + C::BM * C::KB, w, lane);
-  }
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + C::S - 2 < nk) wait_vm<(C::S - 2) * kCopies>();
-    else wait_vm<0>();
-    __syncthreads();
-    if (kt + C::S - 1 < nk) {
-      char* st = smem + ((kt + C::S - 1) % C::S) * C::kStage;
-      p.issue(g, t, kt + C::S - 1, st, st + C::BM * C::KB, w, lane);
+    for (int j = 0; j < C::S - 1; ++j) {
+      char* st = smem + j * C::kStage;
+      if (j < nk) p.issue(g, t, j, st, st + C::BM * C::KB, w, lane);
     }
-    char* cur = smem + (kt % C::S) * C::kStage;
-    mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt + C::S - 2 < nk) wait_vm<(C::S - 2) * kCopies>();
+      else wait_vm<0>();
+      // A bare s_barrier: __syncthreads() would add a memory fence, for which
+      // the compiler waits for every copy in flight (vmcnt(0)) and so defeats
+      // the deeper stages.  The explicit wait above already makes this wave's
+      // copies of tile kt visible, and every LDS read of the stage the next
+      // copy overwrites has returned (its MFMA has issued).
+      __builtin_amdgcn_s_barrier();
+      if (kt + C::S - 1 < nk) {
+        char* st = smem + ((kt + C::S - 1) % C::S) * C::kStage;
+        p.issue(g, t, kt + C::S - 1, st, st + C::BM * C::KB, w, lane);
+      }
+      char* cur = smem + (kt % C::S) * C::kStage;
+      mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
+    }
+  } else {
+    // Register-staged double buffer: the loads of tile kt + 1 are in flight
+    // while tile kt is multiplied, then written to the stage that tile kt - 1
+    // used (free since the barrier that opened this step).
+    static_assert(C::S == 2, "register staging uses two LDS stages");
+    if (nk > 0) {
+      p.issue(g, t, 0, smem, smem + C::BM * C::KB, w, lane);
+      wait_vm<0>();
+      p.commit(smem, smem + C::BM * C::KB, w, lane);
+    }
+    for (int kt = 0; kt < nk; ++kt) {
+      __syncthreads();
+      char* cur = smem + (kt & 1) * C::kStage;
+      char* nxt = smem + ((kt + 1) & 1) * C::kStage;
+      const bool more = kt + 1 < nk;
+      if (more) p.issue(g, t, kt + 1, nxt, nxt + C::BM * C::KB, w, lane);
+      mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
+      if (more) {
+        wait_vm<0>();
+        p.commit(nxt, nxt + C::BM * C::KB, w, lane);
+      }
+    }
   }
   p.epilogue(g, t, acc, wm, wn, lane);
 }
@@ -943,10 +1043,26 @@ inline double rounds(int tiles, int per_cu) {
 }
 
 using Big8 = Cfg<256, 256, 2, 4, 2>;        // 8 waves of 128 x 64
+using Big8R = Cfg<256, 256, 2, 4, 2, 128, 0>;  // Big8 with register-staged copies
+using BigR = Cfg<256, 256, 2, 2, 2, 128, 0>;   // Big with register-staged copies
 using Big8S4 = Cfg<256, 256, 2, 4, 4, 64>;  // half-depth K tiles, 4 stages
 using Big8S5 = Cfg<256, 256, 2, 4, 5, 64>;  // half-depth K tiles, 5 stages
 using SmallS4 = Cfg<128, 128, 2, 2, 4, 64>;
 using SmallS3 = Cfg<128, 128, 2, 2, 3, 64>;
+
+// Operand copy path per problem: the dgrads (an activation-row operand and a
+// K-strided weight operand) measured 8-16 % faster with register-staged
+// copies; the forward GEMMs and the weight gradients are faster with direct
+// copies into LDS.
+template <template <typename, class> class PT> struct StagedCopies {
+  static constexpr bool value = false;
+};
+template <> struct StagedCopies<ProbFC2Dgrad> {
+  static constexpr bool value = true;
+};
+template <> struct StagedCopies<ProbFC1Dgrad> {
+  static constexpr bool value = true;
+};
 
 // Pick the tile shape.  The 256 x 256 tile on 8 waves (one workgroup per CU,
 // two waves per SIMD, 128 x 64 per wave) measured fastest on every workload
@@ -963,9 +1079,14 @@ hipError_t launch_auto(const GemmArgs& g, hipStream_t s) {
     case 5: return launch_cfg<PT, Big8S5>(g, s);
     case 6: return launch_cfg<PT, SmallS4>(g, s);
     case 7: return launch_cfg<PT, SmallS3>(g, s);
+    case 8: return launch_cfg<PT, Big8R>(g, s);
+    case 9: return launch_cfg<PT, BigR>(g, s);
     default: break;
   }
-  if (PT<float, Big8>::grid(g) >= 128) return launch_cfg<PT, Big8>(g, s);
+  if (PT<float, Big8>::grid(g) >= 128) {
+    if constexpr (StagedCopies<PT>::value) return launch_cfg<PT, Big8R>(g, s);
+    else return launch_cfg<PT, Big8>(g, s);
+  }
   return launch_cfg<PT, Small>(g, s);
 }
 
