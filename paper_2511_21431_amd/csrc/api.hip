@@ -226,6 +226,32 @@ bool pair_launches() {
   return v;
 }
 
+// MEMFINE_SPLIT=0 keeps the last, partial round of a row-grouped GEMM in
+// full-size tiles (default 1: quarter tiles when it is at most half full).
+int split_tail() {
+  static const int v = [] {
+    const char* e = getenv("MEMFINE_SPLIT");
+    return (e && atoi(e) == 0) ? 0 : 1;
+  }();
+  return v;
+}
+
+// Compute units of the current device (cached per device id).
+int device_cus() {
+  static std::mutex mu;
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  std::lock_guard<std::mutex> lk(mu);
+  if (cache[dev] == 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+      v = 256;
+    cache[dev] = v;
+  }
+  return cache[dev];
+}
+
 int hip_status(hipError_t e) { return e == hipSuccess ? MEMFINE_OK : MEMFINE_ERR_HIP; }
 
 GemmArgs gemm_args(const memfine_shape& s, int64_t n, const ChunkBuffers& c) {
@@ -249,6 +275,8 @@ GemmArgs gemm_args(const memfine_shape& s, int64_t n, const ChunkBuffers& c) {
   g.T_h_bytes = s.T * (int64_t)s.h * elem_bytes(s);
   g.tile_override = tile_override();
   g.raster = raster_mode();
+  g.cus = device_cus();
+  g.split_tail = split_tail();
   return g;
 }
 

@@ -394,6 +394,39 @@ __device__ __forceinline__ bool locate_rows(const int32_t* __restrict__ offsets,
   return false;
 }
 
+// Row-grouped problems: output tiles of BM rows x BNU columns (P::ncols(g)
+// columns in all), reduction length P::reduction(g).
+template <class P, int BM, int BNU>
+__device__ __forceinline__ bool locate_row_tile(const GemmArgs& g, Tile& t, int id, int n) {
+  const int ntn = (P::ncols(g) + BNU - 1) / BNU;
+  int mt, nt;
+  tile_coords(g.raster, id, n, n / ntn, ntn, mt, nt);
+  if (!locate_rows<BM>(g.offsets, g.E, mt, t)) return false;
+  t.n0 = nt * BNU;
+  t.K = P::reduction(g);
+  return true;
+}
+// Quarter `sub` (2 x 2) of tile b of the grid with twice the tile size
+// (2 BM x 2 BNU, row-major order): the split tail of a launch.
+template <class P, int BM, int BNU>
+__device__ __forceinline__ bool locate_row_subtile(const GemmArgs& g, Tile& t, int b, int sub) {
+  const int ntn2 = (P::ncols(g) + 2 * BNU - 1) / (2 * BNU);
+  const int mt = b / ntn2, nt = b % ntn2;
+  if (!locate_rows<2 * BM>(g.offsets, g.E, mt, t)) return false;
+  const int sm = sub >> 1, sn = sub & 1;
+  t.m0 += sm * BM;
+  t.mrows = min(t.mrows - sm * BM, BM);
+  t.n0 = (2 * nt + sn) * BNU;
+  t.K = P::reduction(g);
+  return t.mrows > 0 && t.n0 < P::ncols(g);
+}
+// Exact number of row-grouped m-tiles of BM rows: sum over experts of ceil(c_e / BM).
+template <int BM> __device__ __forceinline__ int row_tiles(const int32_t* __restrict__ offsets, int E) {
+  int n = 0;
+  for (int e = 0; e < E; ++e) n += (offsets[e + 1] - offsets[e] + BM - 1) / BM;
+  return n;
+}
+
 template <typename T> __device__ __forceinline__ const char* cptr(const void* base, int64_t el) {
   return (const char*)base + el * (int64_t)sizeof(T);
 }
@@ -438,23 +471,24 @@ __device__ __forceinline__ void store_rows(const Accum<C>& acc, T* out, int ld, 
 //   dgp[m, f / 32] = sum over 32 columns f of dA a    (gate-gradient partials)
 // Each dA element is read and then overwritten by the one lane that owns it.
 template <typename T, class C, bool kBwd> struct ProbFC1 {
+  typedef ProbFC1 ProbSelf;
   static constexpr int kHalf = C::WTN / 2;
   typedef KcOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
   typedef KcOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
   OA A;
   OB B;
   static int grid(const GemmArgs& g) {
-    return row_tiles_bound(g.n, g.E, C::BM) * ((g.F + C::BN / 2 - 1) / (C::BN / 2));
+    return row_tiles_bound(g.n, g.E, C::BM) * ((ncols(g) + BNU - 1) / BNU);
   }
+  static constexpr int BNU = C::BN / 2;  // output columns per tile
+  __host__ __device__ static int ncols(const GemmArgs& g) { return g.F; }
   __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t, int id, int n) const {
-    const int ntn = (g.F + C::BN / 2 - 1) / (C::BN / 2);
-    int mt, nt;
-    tile_coords(g.raster, id, n, n / ntn, ntn, mt, nt);
-    if (!locate_rows<C::BM>(g.offsets, g.E, mt, t)) return false;
-    t.n0 = nt * (C::BN / 2);
-    t.K = g.h;
-    return true;
+    return locate_row_tile<ProbSelf, C::BM, BNU>(g, t, id, n);
   }
+  __device__ __forceinline__ bool locate_sub(const GemmArgs& g, Tile& t, int b, int sub) const {
+    return locate_row_subtile<ProbSelf, C::BM, BNU>(g, t, b, sub);
+  }
+  __host__ __device__ static int reduction(const GemmArgs& g) { return g.h; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
     A.rs = make_rsrc(g.X, g.T_h_bytes);
     const int32_t* tok = g.tok_of_row + t.m0;
@@ -580,22 +614,23 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
 
 // Forward FC2: y[m, n] = sum_f a[m, f] W2[e, n, f].     K = F
 template <typename T, class C> struct ProbFC2 {
+  typedef ProbFC2 ProbSelf;
   typedef KcOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
   typedef KcOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
   OA A;
   OB B;
   static int grid(const GemmArgs& g) {
-    return row_tiles_bound(g.n, g.E, C::BM) * ((g.h + C::BN - 1) / C::BN);
+    return row_tiles_bound(g.n, g.E, C::BM) * ((ncols(g) + BNU - 1) / BNU);
   }
+  static constexpr int BNU = C::BN;  // output columns per tile
+  __host__ __device__ static int ncols(const GemmArgs& g) { return g.h; }
   __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t, int id, int n) const {
-    const int ntn = (g.h + C::BN - 1) / C::BN;
-    int mt, nt;
-    tile_coords(g.raster, id, n, n / ntn, ntn, mt, nt);
-    if (!locate_rows<C::BM>(g.offsets, g.E, mt, t)) return false;
-    t.n0 = nt * C::BN;
-    t.K = g.F;
-    return true;
+    return locate_row_tile<ProbSelf, C::BM, BNU>(g, t, id, n);
   }
+  __device__ __forceinline__ bool locate_sub(const GemmArgs& g, Tile& t, int b, int sub) const {
+    return locate_row_subtile<ProbSelf, C::BM, BNU>(g, t, b, sub);
+  }
+  __host__ __device__ static int reduction(const GemmArgs& g) { return g.F; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
     const uint32_t rowb = (uint32_t)g.F * sizeof(T);
     A.rs = make_rsrc(cptr<T>(g.a, (int64_t)t.m0 * g.F), (int64_t)t.mrows * rowb);
@@ -625,24 +660,24 @@ template <typename T, class C> struct ProbFC2 {
 // Backward FC2 dgrad: dA[m, f] = sum_o dY[tok(m), o] W2[e, o, f]     K = h
 // (written to `ag`; the SwiGLU backward happens in the FC1 recomputation).
 template <typename T, class C> struct ProbFC2Dgrad {
+  typedef ProbFC2Dgrad ProbSelf;
   typedef KcOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
   typedef KsOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
   OA A;
   OB B;
   uint32_t b_ktile;  // bytes of W2 per K tile (BK rows)
   static int grid(const GemmArgs& g) {
-    return row_tiles_bound(g.n, g.E, C::BM) * ((g.F + C::BN - 1) / C::BN);
+    return row_tiles_bound(g.n, g.E, C::BM) * ((ncols(g) + BNU - 1) / BNU);
   }
+  static constexpr int BNU = C::BN;  // output columns per tile
+  __host__ __device__ static int ncols(const GemmArgs& g) { return g.F; }
   __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t, int id, int n) const {
-    const int ntn = (g.F + C::BN - 1) / C::BN;
-    int mt, nt;
-    tile_coords(g.raster, id, n, n / ntn, ntn, mt, nt);
-    if (!locate_rows<C::BM>(g.offsets, g.E, mt, t)) return false;
-    t.n0 = nt * C::BN;
-    t.K = g.h;
-    return true;
+    return locate_row_tile<ProbSelf, C::BM, BNU>(g, t, id, n);
   }
-  __device__ __forceinline__ static int reduction(const GemmArgs& g) { return g.h; }
+  __device__ __forceinline__ bool locate_sub(const GemmArgs& g, Tile& t, int b, int sub) const {
+    return locate_row_subtile<ProbSelf, C::BM, BNU>(g, t, b, sub);
+  }
+  __host__ __device__ static int reduction(const GemmArgs& g) { return g.h; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
     A.rs = make_rsrc(g.dY, g.T_h_bytes);
     const int32_t* tok = g.tok_of_row + t.m0;
@@ -678,24 +713,24 @@ template <typename T, class C> struct ProbFC2Dgrad {
 
 // Backward FC1 dgrad: dxp[m, n] = sum_c du[m, c] W1[e, c, n].    K = 2F
 template <typename T, class C> struct ProbFC1Dgrad {
+  typedef ProbFC1Dgrad ProbSelf;
   typedef KcOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
   typedef KsOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
   OA A;
   OB B;
   uint32_t b_ktile;
   static int grid(const GemmArgs& g) {
-    return row_tiles_bound(g.n, g.E, C::BM) * ((g.h + C::BN - 1) / C::BN);
+    return row_tiles_bound(g.n, g.E, C::BM) * ((ncols(g) + BNU - 1) / BNU);
   }
+  static constexpr int BNU = C::BN;  // output columns per tile
+  __host__ __device__ static int ncols(const GemmArgs& g) { return g.h; }
   __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t, int id, int n) const {
-    const int ntn = (g.h + C::BN - 1) / C::BN;
-    int mt, nt;
-    tile_coords(g.raster, id, n, n / ntn, ntn, mt, nt);
-    if (!locate_rows<C::BM>(g.offsets, g.E, mt, t)) return false;
-    t.n0 = nt * C::BN;
-    t.K = 2 * g.F;
-    return true;
+    return locate_row_tile<ProbSelf, C::BM, BNU>(g, t, id, n);
   }
-  __device__ __forceinline__ static int reduction(const GemmArgs& g) { return 2 * g.F; }
+  __device__ __forceinline__ bool locate_sub(const GemmArgs& g, Tile& t, int b, int sub) const {
+    return locate_row_subtile<ProbSelf, C::BM, BNU>(g, t, b, sub);
+  }
+  __host__ __device__ static int reduction(const GemmArgs& g) { return 2 * g.F; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
     const uint32_t rowb = (uint32_t)2 * g.F * sizeof(T);
     A.rs = make_rsrc(cptr<T>(g.u, (int64_t)t.m0 * 2 * g.F), (int64_t)t.mrows * rowb);
@@ -906,10 +941,7 @@ template <int N> __device__ __forceinline__ void wait_vm() {
 // publishes every wave's copies and also certifies that all waves are done
 // with tile kt-1, whose stage the next copy overwrites.
 template <typename T, class C, class P>
-__device__ __forceinline__ void run_tile(const GemmArgs& g, char* smem, int id, int n) {
-  P p;
-  Tile t;
-  if (!p.locate(g, t, id, n)) return;
+__device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p, const Tile& t) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w / C::WN, wn = w % C::WN;
   p.init(g, t, w, lane);
   Accum<C> acc;
@@ -966,10 +998,48 @@ __device__ __forceinline__ void run_tile(const GemmArgs& g, char* smem, int id, 
 }
 
 template <typename T, class C, class P>
+__device__ __forceinline__ void run_tile(const GemmArgs& g, char* smem, int id, int n) {
+  P p;
+  Tile t;
+  if (p.locate(g, t, id, n)) run_located<T, C, P>(g, smem, p, t);
+}
+
+template <typename T, class C, class P>
 __global__ __launch_bounds__(C::kThreads, C::kMinWaves)
 __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_gemm_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(1024))) char smem[C::kLds];
   run_tile<T, C, P>(g, smem, blockIdx.x, gridDim.x);
+}
+
+// Row-grouped problem with a split tail.  Tiles of configuration C fill the
+// full rounds (floor(tiles / cus) * cus of them); when the last, partial
+// round would hold at most cus / 2 tiles, each of its tiles runs instead as
+// four quarter tiles of configuration CQ (same workgroup size), spread over
+// four times as many CUs, so the launch ends about three quarters of a
+// round earlier.  The tile count depends on the chunk's expert offsets and is
+// computed here; workgroups past the work exit at once.
+template <typename T, class C, class CQ, class P, class PQ>
+__global__ __launch_bounds__(C::kThreads, C::kMinWaves)
+__attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_gemm_split_kernel(
+    GemmArgs g) {
+  static_assert(C::kThreads == CQ::kThreads && C::kLds >= CQ::kLds, "quarter tiles must fit");
+  static_assert(CQ::BM * 2 == C::BM && PQ::BNU * 2 == P::BNU, "quarter tiles of the same grid");
+  __shared__ __attribute__((aligned(1024))) char smem[C::kLds];
+  const int ntn = (P::ncols(g) + P::BNU - 1) / P::BNU;
+  const int tiles = row_tiles<C::BM>(g.offsets, g.E) * ntn;
+  const int full = tiles / g.cus * g.cus, rem = tiles - full;
+  const bool split = 2 * rem <= g.cus;
+  const int id = blockIdx.x;
+  if (id < full || (!split && id < tiles)) {
+    P p;
+    Tile t;
+    if (p.locate(g, t, id, tiles)) run_located<T, C, P>(g, smem, p, t);
+  } else if (split && id < full + 4 * rem) {
+    PQ p;
+    Tile t;
+    const int q = id - full;
+    if (p.locate_sub(g, t, full + q / 4, q % 4)) run_located<T, CQ, PQ>(g, smem, p, t);
+  }
 }
 
 // The dgrad and the wgrad of one FC layer in one launch (nd + nw workgroups;
@@ -1045,10 +1115,38 @@ inline double rounds(int tiles, int per_cu) {
 using Big8 = Cfg<256, 256, 2, 4, 2>;        // 8 waves of 128 x 64
 using Big8R = Cfg<256, 256, 2, 4, 2, 128, 0>;  // Big8 with register-staged copies
 using BigR = Cfg<256, 256, 2, 2, 2, 128, 0>;   // Big with register-staged copies
+using Quarter8 = Cfg<128, 128, 4, 2, 2>;        // quarter tiles of Big8 (8 waves of 32 x 64)
+using Quarter8R = Cfg<128, 128, 4, 2, 2, 128, 0>;
 using Big8S4 = Cfg<256, 256, 2, 4, 4, 64>;  // half-depth K tiles, 4 stages
 using Big8S5 = Cfg<256, 256, 2, 4, 5, 64>;  // half-depth K tiles, 5 stages
 using SmallS4 = Cfg<128, 128, 2, 2, 4, 64>;
 using SmallS3 = Cfg<128, 128, 2, 2, 3, 64>;
+
+template <typename T, class C> using FC1Fwd = ProbFC1<T, C, false>;
+template <typename T, class C> using FC1Bwd = ProbFC1<T, C, true>;
+template <typename T, class C> using FC2W = ProbWgrad<T, C, false>;
+template <typename T, class C> using FC1W = ProbWgrad<T, C, true>;
+
+// Row-grouped problems (tiles over the chunk's rows) can split their tail.
+template <template <typename, class> class PT> struct RowGrouped {
+  static constexpr bool value = true;
+};
+template <> struct RowGrouped<FC2W> {
+  static constexpr bool value = false;
+};
+template <> struct RowGrouped<FC1W> {
+  static constexpr bool value = false;
+};
+
+template <template <typename, class> class PT, class C, class CQ>
+hipError_t launch_split_cfg(const GemmArgs& g, hipStream_t s) {
+  const int bound = PT<bf16_t, C>::grid(g);
+  if (bound <= 0) return hipSuccess;
+  const int blocks = bound + 3 * (g.cus / 2);
+  grouped_gemm_split_kernel<bf16_t, C, CQ, PT<bf16_t, C>, PT<bf16_t, CQ>>
+      <<<blocks, C::kThreads, 0, s>>>(g);
+  return hipGetLastError();
+}
 
 // Operand copy path per problem: the dgrads (an activation-row operand and a
 // K-strided weight operand) measured 8-16 % faster with register-staged
@@ -1084,6 +1182,12 @@ hipError_t launch_auto(const GemmArgs& g, hipStream_t s) {
     default: break;
   }
   if (PT<float, Big8>::grid(g) >= 128) {
+    if constexpr (RowGrouped<PT>::value) {
+      if (g.split_tail && g.raster == 0) {
+        if constexpr (StagedCopies<PT>::value) return launch_split_cfg<PT, Big8R, Quarter8R>(g, s);
+        else return launch_split_cfg<PT, Big8, Quarter8>(g, s);
+      }
+    }
     if constexpr (StagedCopies<PT>::value) return launch_cfg<PT, Big8R>(g, s);
     else return launch_cfg<PT, Big8>(g, s);
   }
@@ -1097,10 +1201,6 @@ hipError_t launch_pair(const GemmArgs& g, hipStream_t s) {
   return launch_pair_cfg<P1, P2, Big8>(g, s);
 }
 
-template <typename T, class C> using FC1Fwd = ProbFC1<T, C, false>;
-template <typename T, class C> using FC1Bwd = ProbFC1<T, C, true>;
-template <typename T, class C> using FC2W = ProbWgrad<T, C, false>;
-template <typename T, class C> using FC1W = ProbWgrad<T, C, true>;
 
 }  // namespace
 

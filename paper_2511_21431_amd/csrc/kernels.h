@@ -66,6 +66,8 @@ struct GemmArgs {
   int64_t T_h_bytes; // bytes of X (and of dY): T * h * element size
   int tile_override; // 0: choose the tile shape per problem; else a fixed shape
   int raster;        // tile traversal: 0 row-major, 1..3 XCD-grouped (group 4, 8, 16)
+  int cus;           // compute units of the device
+  int split_tail;    // 1: row-grouped GEMMs run a short last round as quarter tiles
 };
 
 int dgate_partials(int F);

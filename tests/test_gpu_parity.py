@@ -248,6 +248,31 @@ def test_out_of_range_ids_are_dropped(mf):
         assert np.all(host(B["dgates"])[drop] == 0.0)
 
 
+def test_split_tail_parity(mf):
+    """A shape whose grids run on 256 x 256 tiles with a short last round
+    (FC1: 68 m-tiles x 8 = 544 tiles on 256 CUs; FC2 dgrad 272), which the
+    row-grouped GEMMs run as quarter tiles: checked in full against the oracle,
+    and Y / dX / dgates bit-identical between C = 1 and C = 2 (whose grids
+    split differently)."""
+    w = mw.scaled(W[2], T=4096, h=512, F=1024, E=8)
+    case = mw.make_case(w, 211)
+    dev = device_case(w, case)
+    res = {}
+    for C in (1, 2):
+        log(f"split tail C={C}")
+        Y = host(run_fwd(w, dev, C))
+        B = {k: host(v) for k, v in run_bwd(w, dev, C).items()}
+        res[C] = (Y, B)
+        Y_ref = om.moe_fwd(case["X"], case["idx"], case["gates"], case["W1"], case["W2"], C)
+        R = om.moe_bwd(case["X"], case["idx"], case["gates"], case["W1"], case["W2"], case["dY"], C)
+        assert relerr(Y, Y_ref) <= TOL["bf16"]
+        for key in ("dX", "dgates", "dW1", "dW2"):
+            assert relerr(B[key], R[key]) <= TOL["bf16"], (C, key)
+    assert np.array_equal(res[1][0], res[2][0])
+    for key in ("dX", "dgates"):
+        assert np.array_equal(res[1][1][key], res[2][1][key]), key
+
+
 def test_allocator_hook_peak_and_oom(mf):
     """The working memory the layer holds at once, measured two ways (the
     allocator hook's own high-water mark, and torch's allocator statistics),
