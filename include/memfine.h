@@ -163,6 +163,64 @@ int memfine_plan(const memfine_shape* shape, const int64_t* h_counts, int64_t bu
  */
 int64_t memfine_workspace_bytes(const memfine_shape* shape, int32_t chunks, int32_t pass);
 
+/* ------------------------------------------------------------------------
+ * MACT from the model configuration (paper Section 3 and Section 4.2).
+ * Pure host arithmetic, exact (128-bit integers); no device state.
+ *
+ * The memory model uses the symbols of the paper's notation table; every
+ * size is an element count and D_t the bytes per activation element.
+ */
+typedef struct memfine_model {
+  int64_t b, s;            /* micro-batch size, sequence length                */
+  int64_t h, a, h_d, k_a;  /* hidden size, heads, head dim, kv heads           */
+  int64_t e_n, g_e;        /* router output width, expert FFN size (F)         */
+  int32_t t, c;            /* tensor- and context-parallel sizes (>= 1)        */
+  int32_t v, p;            /* pipeline stages per GPU, pipeline size (>= 1)    */
+  int32_t D_t;             /* activation bytes per element (>= 1)              */
+  int32_t full_recompute;  /* 1: m_g = 1; 0: m_g = v p + p - 2 r_pp - 1        */
+} memfine_model;
+
+/*
+ * Eq. (1): static memory = (D_para + D_grad + 4 D_opt) * v * l * sum(S_para),
+ * parameters, gradients and four optimizer-state copies of the m_n weighted
+ * modules of a layer (S_para[i] elements each), v stages of l layers.
+ * *bytes_out receives the total.  MEMFINE_ERR_INVALID_ARG on a negative or
+ * zero size factor, a negative S_para, or a result beyond int64.
+ */
+int memfine_static_memory(const int64_t* S_para, int32_t m_n, int32_t v, int32_t l,
+                          int32_t D_para, int32_t D_grad, int32_t D_opt, int64_t* bytes_out);
+
+/*
+ * Eq. (2): peak activation bytes at pipeline rank r_pp (0 <= r_pp < p) with
+ * s_recv received slots, m_g/(t c) D_t b (s (5h + a h_d + 2 k_a h_d + e_n)
+ * + s_recv (2h + 2 g_e)), rounded up to whole bytes.  With chunking, s_recv
+ * is the largest chunk's slots.  MEMFINE_ERR_INVALID_ARG on invalid fields,
+ * m_g < 1, or a result beyond int64.
+ */
+int memfine_activation_memory(const memfine_model* m, int32_t r_pp, int64_t s_recv,
+                              int64_t* bytes_out);
+
+/*
+ * MACT set-up, once per pipeline rank before training: the threshold table
+ * of the bins.  s'_max is Eq. (8) with alpha = alpha_num / alpha_den, GPU
+ * memory M_gpu and static memory M_sta (bytes); thresholds_out[i] is the
+ * largest s'' for which bins[i] chunks keep Eq. (3), floor(bins[i] * s'_max),
+ * or -1 when the part of Eq. (2) that does not depend on s'' alone exceeds
+ * alpha M_gpu - M_sta.  Values beyond int64 are clamped to INT64_MAX.
+ */
+int memfine_mact_thresholds(const memfine_model* m, int32_t r_pp, int64_t M_gpu, int64_t alpha_num,
+                            int64_t alpha_den, int64_t M_sta, const int32_t* bins, int32_t nbins,
+                            int64_t* thresholds_out);
+
+/*
+ * MACT at run time, per iteration and layer: the smallest bin whose
+ * threshold admits the received slots s_recv (the threshold form of Eq. (9)
+ * followed by the bin choice).  When no bin admits them, *chunks_out is the
+ * largest bin and the call returns MEMFINE_ERR_BUDGET.
+ */
+int memfine_mact_select(const int32_t* bins, const int64_t* thresholds, int32_t nbins,
+                        int64_t s_recv, int32_t* chunks_out);
+
 /*
  * Chunked forward, Eq. (6): Y = concat(F_w(X_1), ..., F_w(X_C)), with
  * F_w = combine(expert(dispatch(.))) of Eq. (4) on tokens

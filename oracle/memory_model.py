@@ -18,6 +18,9 @@ Passages followed
 * Section 4.2, Eq. (8): s'_max, the most received slots the budget allows;
   Eq. (9): c = ceil(s'' / s'_max); then the chunk count is taken from a set of
   bins.
+* Section 4.2, threshold method: before training, each pipeline stage turns
+  Eq. (8) into one s'' threshold per bin; at run time the chunk count is the
+  smallest bin whose threshold admits the received slots.
 * Section 4.1: the chunked layer's peak is the largest chunk's activation.
 
 Readings (the paper is ambiguous here)
@@ -35,14 +38,17 @@ Readings (the paper is ambiguous here)
 Pins: Table 2's rows must add up to its printed Total row and to Eq. (2);
 the Table 4 percentages printed in Section 5 (48.03 %, 83.84 %); the 1/C
 scaling of the chunked MoE term against Table 4's three activation figures;
-hand-worked Eq. (8)/(9) tables.  The absolute 22.9 GB of Table 4 is parity
-unpinned: the received-slot count and the attention shapes of that run are
-not printed.
+hand-worked Eq. (8)/(9) tables; the threshold method selects, for every s'',
+the same bin as Eq. (9) followed by the bin choice, and that bin keeps Eq. (3)
+while the next smaller one breaks it.  The absolute 22.9 GB of Table 4 is
+parity unpinned: the received-slot count and the attention shapes of that
+run are not printed.  Eq. (1) is parity unpinned as well: the per-module
+weight sizes behind Table 4's static memory are not printed.
 """
 from __future__ import annotations
 
 from fractions import Fraction
-from typing import Dict, Iterable, Optional, Sequence, Tuple
+from typing import List, Dict, Iterable, Optional, Sequence, Tuple
 
 
 def _F(x) -> Fraction:
@@ -142,6 +148,29 @@ def plan(counts: Sequence[int], budget: int, beta: int,
     c = theoretical_chunks(s2, smax)
     C, ok = select_bin(c, bins)
     return {"C": C, "ok": ok, "c_theory": c, "s2": s2, "s_max": smax}
+
+
+# --- MACT's threshold method (Section 4.2) ---------------------------------------
+def mact_thresholds(smax: Fraction, bins: Sequence[int]) -> List[int]:
+    """Before training, per pipeline stage: for every bin, the largest s''
+    that the bin's chunk count keeps within Eq. (3).  Splitting s'' received
+    slots into b chunks leaves s''/b of them live, so bin b admits s'' while
+    s''/b <= s'_max, i.e. s'' <= floor(b s'_max); a negative s'_max (the part
+    of Eq. (2) that does not depend on s'' already breaks Eq. (3)) admits
+    nothing (-1)."""
+    smax = _F(smax)
+    if smax < 0:
+        return [-1 for _ in bins]
+    return [int((b * smax).numerator // (b * smax).denominator) for b in bins]
+
+
+def mact_select(bins: Sequence[int], thresholds: Sequence[int], s2: int) -> Tuple[int, bool]:
+    """At run time: the smallest bin whose threshold admits s''; (max(bins),
+    False) when none does."""
+    ok = [b for b, th in zip(bins, thresholds) if s2 <= th]
+    if ok:
+        return min(ok), True
+    return max(bins), False
 
 
 # --- the chunked layer's peak (Section 4.1) -------------------------------------

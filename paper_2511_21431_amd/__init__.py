@@ -4,6 +4,8 @@ The compute lives in libmemfine.so (hand-written gfx950 HIP kernels behind
 the C ABI of include/memfine.h); this package only builds and binds it.
 """
 from ._lib import (BF16, F32, PASS_BWD, PASS_FWD, MemfineError, TorchAllocator,  # noqa: F401
-                   lib, make_shape, memfine_count, memfine_dispatch, memfine_moe_bwd,
-                   memfine_moe_fwd, memfine_plan, memfine_profile_begin, memfine_profile_end,
-                   memfine_status_str, memfine_workspace_bytes)
+                   lib, make_model, make_shape, memfine_activation_memory, memfine_count,
+                   memfine_dispatch, memfine_mact_select, memfine_mact_thresholds,
+                   memfine_moe_bwd, memfine_moe_fwd, memfine_plan, memfine_profile_begin,
+                   memfine_profile_end, memfine_static_memory, memfine_status_str,
+                   memfine_workspace_bytes)

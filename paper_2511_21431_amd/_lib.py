@@ -51,6 +51,15 @@ class PlanInfo(ctypes.Structure):
                 ("paper_peak_bytes", ctypes.c_int64)]
 
 
+class Model(ctypes.Structure):
+    """memfine_model: the memory model's configuration (notation-table symbols)."""
+    _fields_ = [("b", ctypes.c_int64), ("s", ctypes.c_int64), ("h", ctypes.c_int64),
+                ("a", ctypes.c_int64), ("h_d", ctypes.c_int64), ("k_a", ctypes.c_int64),
+                ("e_n", ctypes.c_int64), ("g_e", ctypes.c_int64), ("t", ctypes.c_int32),
+                ("c", ctypes.c_int32), ("v", ctypes.c_int32), ("p", ctypes.c_int32),
+                ("D_t", ctypes.c_int32), ("full_recompute", ctypes.c_int32)]
+
+
 class KernelStat(ctypes.Structure):
     _fields_ = [("launches", ctypes.c_int64), ("total_ms", ctypes.c_double),
                 ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
@@ -72,6 +81,14 @@ _SIGS = {
     "memfine_moe_fwd": (ctypes.c_int, [SHP, ctypes.c_int32, P, P, P, P, P, P, ALP, P]),
     "memfine_moe_bwd": (ctypes.c_int, [SHP, ctypes.c_int32, P, P, P, P, P, P, P, P, P, P,
                                        ctypes.c_int32, ALP, P]),
+    "memfine_static_memory": (ctypes.c_int, [I64P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                             ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, I64P]),
+    "memfine_activation_memory": (ctypes.c_int, [ctypes.POINTER(Model), ctypes.c_int32,
+                                                 ctypes.c_int64, I64P]),
+    "memfine_mact_thresholds": (ctypes.c_int, [ctypes.POINTER(Model), ctypes.c_int32, ctypes.c_int64,
+                                               ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, I32P,
+                                               ctypes.c_int32, I64P]),
+    "memfine_mact_select": (ctypes.c_int, [I32P, I64P, ctypes.c_int32, ctypes.c_int64, I32P]),
     "memfine_status_str": (ctypes.c_char_p, [ctypes.c_int]),
     "memfine_profile_begin": (ctypes.c_int, [ctypes.c_uint32]),
     "memfine_profile_end": (ctypes.c_int, [ctypes.POINTER(KernelStat)]),
@@ -222,6 +239,60 @@ def memfine_plan(shape: Shape, counts: Sequence[int], budget_bytes: int, bins=(1
                             ctypes.byref(out), ctypes.byref(info))
     _check(rc, "memfine_plan", allow=(OK, ERR_BUDGET))
     return rc, int(out.value), {f: getattr(info, f) for f, _ in PlanInfo._fields_}
+
+
+def make_model(**kw) -> Model:
+    """memfine_model from keyword fields (b, s, h, a, h_d, k_a, e_n, g_e, t, c, v, p,
+    D_t, full_recompute); unspecified fields default to 0 except the parallel
+    sizes and b (1), D_t (2) and full_recompute (1)."""
+    d = dict(b=1, t=1, c=1, v=1, p=1, D_t=2, full_recompute=1)
+    d.update(kw)
+    m = Model()
+    for f, _ in Model._fields_:
+        setattr(m, f, int(d.get(f, 0)))
+    return m
+
+
+def memfine_static_memory(S_para: Sequence[int], v: int, l: int, D_para: int = 2,
+                          D_grad: int = 2, D_opt: int = 4) -> int:
+    a = np.ascontiguousarray(np.asarray(list(S_para), dtype=np.int64))
+    out = ctypes.c_int64(0)
+    rc = lib().memfine_static_memory(a.ctypes.data_as(I64P), int(a.size), int(v), int(l),
+                                     int(D_para), int(D_grad), int(D_opt), ctypes.byref(out))
+    _check(rc, "memfine_static_memory")
+    return int(out.value)
+
+
+def memfine_activation_memory(model: Model, r_pp: int, s_recv: int) -> int:
+    out = ctypes.c_int64(0)
+    rc = lib().memfine_activation_memory(ctypes.byref(model), int(r_pp), int(s_recv),
+                                         ctypes.byref(out))
+    _check(rc, "memfine_activation_memory")
+    return int(out.value)
+
+
+def memfine_mact_thresholds(model: Model, r_pp: int, M_gpu: int, alpha_num: int, alpha_den: int,
+                            M_sta: int, bins=(1, 2, 4, 8)) -> list:
+    b = np.ascontiguousarray(np.asarray(bins, dtype=np.int32))
+    out = np.zeros(b.size, dtype=np.int64)
+    rc = lib().memfine_mact_thresholds(ctypes.byref(model), int(r_pp), int(M_gpu), int(alpha_num),
+                                       int(alpha_den), int(M_sta), b.ctypes.data_as(I32P),
+                                       int(b.size), out.ctypes.data_as(I64P))
+    _check(rc, "memfine_mact_thresholds")
+    return [int(x) for x in out]
+
+
+def memfine_mact_select(bins: Sequence[int], thresholds: Sequence[int], s_recv: int):
+    """Returns (status, chunks); status is OK or ERR_BUDGET."""
+    b = np.ascontiguousarray(np.asarray(bins, dtype=np.int32))
+    th = np.ascontiguousarray(np.asarray(thresholds, dtype=np.int64))
+    if b.size != th.size:
+        raise ValueError("one threshold per bin")
+    out = ctypes.c_int32(0)
+    rc = lib().memfine_mact_select(b.ctypes.data_as(I32P), th.ctypes.data_as(I64P), int(b.size),
+                                   int(s_recv), ctypes.byref(out))
+    _check(rc, "memfine_mact_select", allow=(OK, ERR_BUDGET))
+    return rc, int(out.value)
 
 
 def memfine_workspace_bytes(shape: Shape, chunks: int, pass_: int) -> int:

@@ -310,7 +310,8 @@ def test_allocator_hook_peak_and_oom(mf):
 
 
 # ---------------------------------------------------- full-size, sampled
-FULL = [(2, 2), (2, 1), (3, 4), (4, 4)]
+# (5, 16): the budget sweep's largest chunk count on its 131072-token batch
+FULL = [(2, 2), (2, 1), (3, 4), (4, 4), (5, 16)]
 
 
 @pytest.mark.parametrize("cfg,C", FULL)
@@ -351,7 +352,12 @@ def test_full_size_sampled(mf, cfg, C):
     errs = {"Y": relerr(host(Y[toks]), Y_ref), "dX": relerr(host(B["dX"][toks]), dX_ref),
             "dgates": relerr(host(B["dgates"][toks]), dg_ref)}
     fs = sorted(set(rng.choice(w.F, size=3, replace=False).tolist()) | {0, w.F - 1})
-    for e in (int(order[0]), int(order[w.E // 2]), int(order[-1])):
+    dw_experts = [int(order[0]), int(order[w.E // 2]), int(order[-1])]
+    if counts[dw_experts[0]] > 20000:
+        # the oracle's column form re-runs the expert's whole forward in fp64:
+        # a 500k-row hot expert is minutes of CPU, so check the others
+        dw_experts = dw_experts[1:]
+    for e in dw_experts:
         g1, u1, c2 = om.moe_dW_expert_columns(X, idx, gates, W1l, W2l, dY, e, fs)
         errs[f"dW1g[{e}]"] = relerr(host(B["dW1"][e][fs]), g1)
         errs[f"dW1u[{e}]"] = relerr(host(B["dW1"][e][[w.F + f for f in fs]]), u1)
