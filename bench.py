@@ -30,6 +30,7 @@ sys.path.insert(0, ROOT)
 import numpy as np  # noqa: E402
 
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+PEAK_HBM_GBS = 8000.0
 HBM_GBS = 8000.0
 
 # activation budget handed to the planner per workload (bytes); the plan
@@ -51,6 +52,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-router", action="store_true",
+                    help="skip the router and block measurement")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target duration of the oracle sample")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -208,6 +211,11 @@ def main():
             })
             log(f"[bench] sweep C={Cs}: {tps:.0f} tokens/s, peak activation {peak_b / 1e9:.3f} GB")
 
+    # ---- the router in front of the layer: its kernels, and the whole block
+    router = None
+    if not args.no_router and w.E <= 64 and w.k <= 16:
+        router = bench_router(mf, torch, w, shape, dev, step, args.steps)
+
     # ---- the oracle on the host cores, bounded sample of the same workload
     cpu = None
     if not args.no_cpu_baseline:
@@ -241,10 +249,79 @@ def main():
                                  "tflops": round(v["flops"] / max(v["total_ms"], 1e-9) / 1e9, 1),
                                  "gbs": round(v["bytes"] / max(v["total_ms"], 1e-9) / 1e6, 1)}
                              for k, v in prof_all.items()},
+        "layer_roofline_frac": round(layer_bound_ms(prof_all, peak) / ms_per_step, 4),
         "chunks_sweep": sweep,
+        "router": router,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def layer_bound_ms(prof, peak_tflops):
+    """Sum over the step's kernels of max(flops / MFMA peak, bytes / HBM peak):
+    the step time at the roofline of every kernel."""
+    return sum(max(v["flops"] / (peak_tflops * 1e12), v["bytes"] / (PEAK_HBM_GBS * 1e9)) * 1e3
+               for v in prof.values())
+
+
+def bench_router(mf, torch, w, shape, dev, layer_step, steps):
+    """Router forward and backward at the workload's shapes (HBM-bound:
+    achieved algorithmic GB/s against 8 TB/s), and the trainable block router
+    -> chunked layer -> layer backward -> router backward in tokens/s."""
+    dt = dev["X"].dtype
+    gen = torch.Generator(device="cuda").manual_seed(4242)
+    Wr = (torch.randn((w.E, w.h), generator=gen, device="cuda") / w.h ** 0.5).to(dt)
+    idx = torch.empty((w.T, w.k), dtype=torch.int32, device="cuda")
+    gates = torch.empty((w.T, w.k), device="cuda")
+    dgr = torch.randn((w.T, w.k), generator=gen, device="cuda")
+    dXr = torch.zeros((w.T, w.h), dtype=dt, device="cuda")
+    dWr = torch.empty((w.E, w.h), device="cuda")
+
+    def fwd_bwd():
+        mf.memfine_router_fwd(shape, dev["X"], Wr, idx, gates)
+        mf.memfine_router_bwd(shape, dev["X"], Wr, idx, gates, dgr, dXr, dWr,
+                              accumulate_dX=True)
+
+    for _ in range(3):
+        fwd_bwd()
+    torch.cuda.synchronize()
+    names = ["router_fwd", "router_bwd_dx", "router_wgrad", "router_reduce"]
+    mf.memfine_profile_begin(names)
+    for _ in range(steps):
+        fwd_bwd()
+    torch.cuda.synchronize()
+    prof = mf.memfine_profile_end()
+    kern = {}
+    for k in names:
+        v = prof.get(k)
+        if not v or not v["launches"]:
+            continue
+        ms = v["total_ms"] / v["launches"]
+        gbs = v["bytes"] / v["launches"] / (ms * 1e-3) / 1e9
+        kern[k] = {"avg_ms": round(ms, 4), "gbs": round(gbs, 1),
+                   "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+                   "tflops": round(v["flops"] / v["launches"] / (ms * 1e-3) / 1e12, 2)}
+    # the block: router forward, layer, router backward into the layer's dX
+    for _ in range(2):
+        fwd_bwd()
+        layer_step()
+    torch.cuda.synchronize()
+    a = time.perf_counter()
+    for _ in range(steps):
+        mf.memfine_router_fwd(shape, dev["X"], Wr, idx, gates)
+        layer_step()
+        mf.memfine_router_bwd(shape, dev["X"], Wr, idx, gates, dgr, dXr, dWr,
+                              accumulate_dX=True)
+    torch.cuda.synchronize()
+    block_s = (time.perf_counter() - a) / steps
+    log(f"[bench] router: " + ", ".join(f"{k} {v['avg_ms']:.4f} ms {v['gbs']:.0f} GB/s"
+                                         for k, v in kern.items())
+        + f"; block {w.T / block_s:.0f} tokens/s")
+    return {"kernels": kern, "block_tokens_per_s": round(w.T / block_s, 1),
+            "block_ms_per_step": round(block_s * 1e3, 4),
+            "note": "router fwd + chunked layer fwd/bwd (same plan as the headline step) + "
+                    "router bwd accumulating into dX; the layer's routing stays the "
+                    "workload's seeded routing"}
 
 
 def cpu_baseline(w, idx_np, gates_np, dev, C, target_s):

@@ -246,6 +246,40 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
                     float* d_dgates, int32_t accumulate_dW, const memfine_allocator* alloc,
                     void* stream);
 
+/* ------------------------------------------------------------------------
+ * Router in front of the expert layer (Table 2 rows 9-10 store its input and
+ * its logits; the gates it produces are the scores that multiply the expert
+ * outputs, Table 2 "score mul").  `shape` is the layer's shape; the router
+ * needs k <= 16 and k <= E <= 64 (MEMFINE_ERR_UNSUPPORTED otherwise).
+ *
+ * Forward: logits = X Wr^T (fp32 accumulation), softmax over the E experts,
+ * the k largest logits (equal logits: the lower expert id first), and the
+ * gates renormalised over the selected k (the full softmax denominator
+ * cancels, so gates_j = exp(z_j - z_max) / sum over the selected).
+ *   d_X       dtype [T, h];   d_Wr  dtype [E, h]
+ *   d_idx     int32 [T, k] out, largest logit first
+ *   d_gates   float [T, k] out
+ *   d_logits  float [T, E] out, may be NULL
+ * Asynchronous; no working memory.
+ */
+int memfine_router_fwd(const memfine_shape* shape, const void* d_X, const void* d_Wr,
+                       int32_t* d_idx, float* d_gates, float* d_logits, void* stream);
+
+/*
+ * Backward from the expert layer's dgates (memfine_moe_bwd's output), with
+ * the selection held fixed: per token, with c = sum_j g_j dg_j,
+ *   dlogits[t, idx_j] = g_j (dg_j - c), 0 for the unselected experts;
+ *   dX  = dlogits Wr   (accumulate_dX = 1 adds it into d_dX, e.g. the
+ *                       layer's dX; 0 overwrites)
+ *   dWr = dlogits^T X  (float [E, h]; accumulate_dWr as above)
+ * Slots whose id lies outside [0, E) pass no gradient.  Working memory
+ * (dense dlogits rows and split-K partials of dWr) comes from `alloc`.
+ */
+int memfine_router_bwd(const memfine_shape* shape, const void* d_X, const void* d_Wr,
+                       const int32_t* d_idx, const float* d_gates, const float* d_dgates,
+                       void* d_dX, float* d_dWr, int32_t accumulate_dX, int32_t accumulate_dWr,
+                       const memfine_allocator* alloc, void* stream);
+
 /* Static, human-readable text for a status code. */
 const char* memfine_status_str(int status);
 
@@ -269,7 +303,11 @@ const char* memfine_status_str(int status);
 #define MEMFINE_K_FC1_DGRAD   9
 #define MEMFINE_K_UNPERMUTE  10   /* dX sum over slots and gate gradient     */
 #define MEMFINE_K_FC1_BWD    11   /* FC1 dgrad and FC1 wgrad in one launch   */
-#define MEMFINE_K_NUM        12
+#define MEMFINE_K_ROUTER_FWD 12   /* router logits, softmax, top-k, gates    */
+#define MEMFINE_K_ROUTER_BWD_DX 13 /* router: dz per token, dX contribution */
+#define MEMFINE_K_ROUTER_WGRAD 14 /* router: split-K partials of dz^T X     */
+#define MEMFINE_K_ROUTER_REDUCE 15 /* router: sum of the partials into dWr  */
+#define MEMFINE_K_NUM        16
 
 typedef struct memfine_kernel_stat {
   int64_t launches;

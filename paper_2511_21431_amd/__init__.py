@@ -7,5 +7,5 @@ from ._lib import (BF16, F32, PASS_BWD, PASS_FWD, MemfineError, TorchAllocator, 
                    lib, make_model, make_shape, memfine_activation_memory, memfine_count,
                    memfine_dispatch, memfine_mact_select, memfine_mact_thresholds,
                    memfine_moe_bwd, memfine_moe_fwd, memfine_plan, memfine_profile_begin,
-                   memfine_profile_end, memfine_static_memory, memfine_status_str,
-                   memfine_workspace_bytes)
+                   memfine_profile_end, memfine_router_bwd, memfine_router_fwd,
+                   memfine_static_memory, memfine_status_str, memfine_workspace_bytes)

@@ -21,7 +21,8 @@ BF16, F32 = 0, 1
 PASS_FWD, PASS_BWD = 0, 1
 
 KERNELS = ["count", "dispatch", "fc1", "fc2", "combine", "fc1_recompute", "fc2_dgrad",
-           "fc2_wgrad", "fc1_wgrad", "fc1_dgrad", "unpermute", "fc1_dgrad_wgrad"]
+           "fc2_wgrad", "fc1_wgrad", "fc1_dgrad", "unpermute", "fc1_dgrad_wgrad",
+           "router_fwd", "router_bwd_dx", "router_wgrad", "router_reduce"]
 
 
 class MemfineError(RuntimeError):
@@ -89,6 +90,9 @@ _SIGS = {
                                                ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, I32P,
                                                ctypes.c_int32, I64P]),
     "memfine_mact_select": (ctypes.c_int, [I32P, I64P, ctypes.c_int32, ctypes.c_int64, I32P]),
+    "memfine_router_fwd": (ctypes.c_int, [SHP, P, P, P, P, P, P]),
+    "memfine_router_bwd": (ctypes.c_int, [SHP, P, P, P, P, P, P, P, ctypes.c_int32,
+                                          ctypes.c_int32, ALP, P]),
     "memfine_status_str": (ctypes.c_char_p, [ctypes.c_int]),
     "memfine_profile_begin": (ctypes.c_int, [ctypes.c_uint32]),
     "memfine_profile_end": (ctypes.c_int, [ctypes.POINTER(KernelStat)]),
@@ -334,6 +338,33 @@ def memfine_moe_bwd(shape: Shape, chunks: int, X, idx, gates, W1, W2, dY, dX, dW
 
 def memfine_status_str(code: int) -> str:
     return status_str(code)
+
+
+def memfine_router_fwd(shape: Shape, X, Wr, idx, gates, logits=None, stream=None) -> None:
+    """Router forward into caller-owned idx [T, k] int32, gates [T, k] fp32 and
+    optionally logits [T, E] fp32."""
+    torch = _torch()
+    dt = _dt(shape)
+    T, h, E, k = shape.T, shape.h, shape.E, shape.k
+    rc = lib().memfine_router_fwd(
+        ctypes.byref(shape), _ptr(X, (T, h), dt, "X"), _ptr(Wr, (E, h), dt, "Wr"),
+        _ptr(idx, (T, k), torch.int32, "idx"), _ptr(gates, (T, k), torch.float32, "gates"),
+        None if logits is None else _ptr(logits, (T, E), torch.float32, "logits"), _stream(stream))
+    _check(rc, "memfine_router_fwd")
+
+
+def memfine_router_bwd(shape: Shape, X, Wr, idx, gates, dgates, dX, dWr, accumulate_dX=False,
+                       accumulate_dWr=False, allocator=None, stream=None) -> None:
+    torch = _torch()
+    dt = _dt(shape)
+    T, h, E, k = shape.T, shape.h, shape.E, shape.k
+    rc = lib().memfine_router_bwd(
+        ctypes.byref(shape), _ptr(X, (T, h), dt, "X"), _ptr(Wr, (E, h), dt, "Wr"),
+        _ptr(idx, (T, k), torch.int32, "idx"), _ptr(gates, (T, k), torch.float32, "gates"),
+        _ptr(dgates, (T, k), torch.float32, "dgates"), _ptr(dX, (T, h), dt, "dX"),
+        _ptr(dWr, (E, h), torch.float32, "dWr"), int(bool(accumulate_dX)),
+        int(bool(accumulate_dWr)), _alloc_arg(allocator), _stream(stream))
+    _check(rc, "memfine_router_bwd")
 
 
 def memfine_profile_begin(kernels: Sequence[str] = tuple(KERNELS)) -> None:

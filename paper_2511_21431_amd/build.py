@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmemfine.so")
 
-SOURCES = ["api.hip", "permute.hip", "combine.hip", "grouped_gemm.hip", "mact.hip"]
+SOURCES = ["api.hip", "permute.hip", "combine.hip", "grouped_gemm.hip", "mact.hip", "router.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -571,6 +571,107 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
   return MEMFINE_OK;
 }
 
+// ------------------------------------------------------------------ router
+namespace {
+constexpr int kRouterEP = 128;  // dense dz row width fed to the split-K wgrad
+
+int check_router(const memfine_shape* shape) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if (shape->k > 16 || shape->k > shape->E || shape->E > 64) return MEMFINE_ERR_UNSUPPORTED;
+  return MEMFINE_OK;
+}
+}  // namespace
+
+int memfine_router_fwd(const memfine_shape* shape, const void* d_X, const void* d_Wr,
+                       int32_t* d_idx, float* d_gates, float* d_logits, void* stream) {
+  int rc = check_router(shape);
+  if (rc) return rc;
+  const memfine_shape& S = *shape;
+  if (S.T == 0) return MEMFINE_OK;
+  if (!d_X || !d_Wr || !d_idx || !d_gates) return MEMFINE_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  const double es = (double)elem_bytes(S), Td = (double)S.T;
+  KernelTimer kt(MEMFINE_K_ROUTER_FWD, s, 2.0 * Td * S.h * S.E,
+                 es * (Td * S.h + (double)S.E * S.h) + 8.0 * Td * S.k +
+                     (d_logits ? 4.0 * Td * S.E : 0.0));
+  return hip_status(launch_router_fwd(S.dtype, d_X, d_Wr, S.T, S.h, S.E, S.k, d_idx, d_gates,
+                                      d_logits, s));
+}
+
+int memfine_router_bwd(const memfine_shape* shape, const void* d_X, const void* d_Wr,
+                       const int32_t* d_idx, const float* d_gates, const float* d_dgates,
+                       void* d_dX, float* d_dWr, int32_t accumulate_dX, int32_t accumulate_dWr,
+                       const memfine_allocator* alloc, void* stream) {
+  int rc = check_router(shape);
+  if (rc) return rc;
+  if ((accumulate_dX != 0 && accumulate_dX != 1) || (accumulate_dWr != 0 && accumulate_dWr != 1))
+    return MEMFINE_ERR_INVALID_ARG;
+  const memfine_shape& S = *shape;
+  if (!d_Wr || !d_dWr) return MEMFINE_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  if (S.T == 0) {
+    if (accumulate_dWr) return MEMFINE_OK;
+    return hip_status(launch_fill_i32((int32_t*)d_dWr, (int64_t)S.E * S.h, 0, s));
+  }
+  if (!d_X || !d_idx || !d_gates || !d_dgates || !d_dX) return MEMFINE_ERR_INVALID_ARG;
+  const int64_t es = elem_bytes(S), T = S.T;
+  // split-K: enough row ranges for about 256 workgroups, each at least 256 rows
+  const int ntn = (S.h + 255) / 256;
+  const int64_t want = (256 + ntn - 1) / ntn, most = std::max<int64_t>(1, T / 256);
+  const int splits = (int)std::max<int64_t>(1, std::min(want, most));
+  const int64_t o_meta = align256(T * kRouterEP * es);
+  const int64_t o_order = o_meta + align256((splits + 1) * 4);
+  const int64_t o_tok = o_order + align256(splits * 4);
+  const int64_t o_part = o_tok + align256(T * 4);
+  const int64_t total = o_part + align256((int64_t)splits * kRouterEP * S.h * 4);
+  char* ws = (char*)ws_alloc(alloc, (size_t)total, s);
+  if (!ws) return MEMFINE_ERR_OOM;
+  void* D = ws;
+  int32_t* offsets = (int32_t*)(ws + o_meta);
+  int32_t* order = (int32_t*)(ws + o_order);
+  int32_t* tok = (int32_t*)(ws + o_tok);
+  float* part = (float*)(ws + o_part);
+  const double Td = (double)T, hd = (double)S.h;
+  hipError_t err;
+  {
+    KernelTimer kt(MEMFINE_K_ROUTER_BWD_DX, s, 2.0 * Td * S.k * hd,
+                   (double)es * (Td * hd * (accumulate_dX ? 2.0 : 1.0) + Td * kRouterEP) + 12.0 * Td * S.k);
+    err = launch_router_bwd_dx(S.dtype, d_Wr, d_idx, d_gates, d_dgates, T, S.h, S.E, S.k,
+                               kRouterEP, accumulate_dX, d_dX, D, s);
+  }
+  if (err == hipSuccess) err = launch_router_split_meta(offsets, order, tok, T, splits, s);
+  if (err == hipSuccess) {
+    // dWr partials: the grouped weight-gradient GEMM over `splits` row ranges
+    // of dz^T X (M = kRouterEP rows of the dense dz, N = h, K = the range)
+    GemmArgs g = {};
+    g.dtype = S.dtype;
+    g.n = (int)T;
+    g.E = splits;
+    g.h = S.h;
+    g.F = kRouterEP / 2;
+    g.offsets = offsets;
+    g.order = order;
+    g.tok_of_row = tok;
+    g.X = d_X;
+    g.u = D;
+    g.dW1 = part;
+    g.accumulate = 0;
+    g.T_h_bytes = T * (int64_t)S.h * es;
+    g.cus = device_cus();
+    KernelTimer kt(MEMFINE_K_ROUTER_WGRAD, s, 2.0 * Td * kRouterEP * hd,
+                   (double)es * (Td * hd + Td * kRouterEP) + 4.0 * splits * kRouterEP * hd);
+    err = launch_fc1_wgrad(g, s);
+  }
+  if (err == hipSuccess) {
+    KernelTimer kt(MEMFINE_K_ROUTER_REDUCE, s, 0.0,
+                   4.0 * (double)S.E * hd * (splits + (accumulate_dWr ? 2.0 : 1.0)));
+    err = launch_router_reduce(part, splits, kRouterEP, S.E, S.h, accumulate_dWr, d_dWr, s);
+  }
+  ws_release(alloc, ws, (size_t)total, s);
+  return hip_status(err);
+}
+
 int memfine_profile_begin(uint32_t mask) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   for (auto& r : g_prof) {

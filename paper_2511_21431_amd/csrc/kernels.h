@@ -72,6 +72,22 @@ struct GemmArgs {
 
 int dgate_partials(int F);
 
+// Router (E <= 64 experts, k <= 16): logits on the matrix cores, softmax,
+// top-k and renormalised gates; logits may be null.
+hipError_t launch_router_fwd(int dtype, const void* X, const void* Wr, int64_t T, int h, int E,
+                             int k, int32_t* idx, float* gates, float* logits, hipStream_t s);
+// Router backward, per token: dX (+)= dz Wr and the dense dz rows D [T, EP].
+hipError_t launch_router_bwd_dx(int dtype, const void* Wr, const int32_t* idx, const float* gates,
+                                const float* dgates, int64_t T, int h, int E, int k, int EP,
+                                int accumulate, void* dX, void* D, hipStream_t s);
+// Row ranges of S splits of T rows (offsets [S + 1], order [S]) and the
+// identity row -> token table [T], for the split-K weight gradient.
+hipError_t launch_router_split_meta(int32_t* offsets, int32_t* order, int32_t* tok, int64_t T, int S,
+                                    hipStream_t s);
+// dWr (+)= sum over the S partial products P [S, EP, h].
+hipError_t launch_router_reduce(const float* P, int S, int EP, int E, int h, int accumulate,
+                                float* dWr, hipStream_t s);
+
 hipError_t launch_fc1_fwd(const GemmArgs& g, hipStream_t s);
 hipError_t launch_fc2_fwd(const GemmArgs& g, hipStream_t s);
 hipError_t launch_fc1_recompute(const GemmArgs& g, hipStream_t s);

@@ -1,0 +1,304 @@
+// Router in front of the expert layer on gfx950: logits = X Wr^T on the
+// matrix cores, softmax, top-k and renormalised gates in registers; the
+// backward's per-token gate-to-logit gradient, its dX contribution, and the
+// reduction of partial weight gradients.  (Table 2 rows 9-10 store the
+// router's input and its logits; the gates are the scores that multiply the
+// expert outputs.)
+#include "common.h"
+#include "kernels.h"
+
+namespace memfine {
+namespace {
+
+constexpr int kRouterWaves = 4;   // 32 tokens per wave, 128 per workgroup
+
+// Per-lane K layout of one K block.  Lane l (row l % 32, half l / 32) holds a
+// contiguous half of its row's block: for bf16 the block is 64 elements and
+// the lane holds elements [32 (l/32), 32 (l/32) + 32) as four 16-byte
+// fragments, fragment s feeding MFMA step s (K 16 split as 8 + 8 over the two
+// lane halves).  A and B use the same map, so each step sums a disjoint part
+// of the block.  For fp32 the block is 32 elements, the lane holds 16 of them
+// and step s takes its s-th element (K 2 split as 1 + 1).
+template <typename T> struct RK;
+template <> struct RK<bf16_t> {
+  static constexpr int KB = 64, STEPS = 4;
+  typedef u32x4_t Raw[4];
+  __device__ __forceinline__ static void load(const bf16_t* row, int kb, int hh, Raw& r) {
+    const u32x4_t* p = (const u32x4_t*)(row + kb * KB + 32 * hh);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) r[s] = p[s];
+  }
+  __device__ __forceinline__ static void mma(const Raw& a, const Raw& b, f32x16_t& c) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, b[s]),
+                                                  __builtin_bit_cast(bf16x8_t, a[s]), c, 0, 0, 0);
+  }
+};
+template <> struct RK<float> {
+  static constexpr int KB = 32, STEPS = 16;
+  typedef f32x4_t Raw[4];
+  __device__ __forceinline__ static void load(const float* row, int kb, int hh, Raw& r) {
+    const f32x4_t* p = (const f32x4_t*)(row + kb * KB + 16 * hh);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) r[s] = p[s];
+  }
+  __device__ __forceinline__ static void mma(const Raw& a, const Raw& b, f32x16_t& c) {
+#pragma unroll
+    for (int s = 0; s < 16; ++s)
+      c = __builtin_amdgcn_mfma_f32_32x32x2f32(b[s >> 2][s & 3], a[s >> 2][s & 3], c, 0, 0, 0);
+  }
+};
+
+// Forward.  Each wave owns 32 tokens x 32 NB experts (NB = 1 or 2); the
+// operands are loaded straight into registers one K block ahead.  After the
+// K loop lane l holds, for token l % 32, the logits of experts
+// 32 nb + 8 (q / 4) + 4 (l / 32) + q % 4 (q = 0..15); lane l ^ 32 holds the
+// token's other half.  Top-k: k rounds, each lane proposes its largest
+// unselected logit (equal: lower id), the two halves compare over one
+// shuffle, the owner marks the winner.
+template <typename T, int NB>
+__global__ __launch_bounds__(64 * kRouterWaves) void router_fwd_kernel(
+    const T* __restrict__ X, const T* __restrict__ Wr, int64_t T_, int h, int E, int k,
+    int32_t* __restrict__ idx, float* __restrict__ gates, float* __restrict__ logits) {
+  typedef RK<T> K;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r = lane & 31, hh = lane >> 5;
+  const int64_t t0 = ((int64_t)blockIdx.x * kRouterWaves + w) * 32;
+  if (t0 >= T_) return;
+  const int64_t trow = min(t0 + r, T_ - 1);  // rows past T read the last row
+  const T* xr = X + trow * h;
+  const T* wr[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) wr[nb] = Wr + (int64_t)min(32 * nb + r, E - 1) * h;
+  f32x16_t acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[nb][q] = 0.f;
+  typename K::Raw a[2], b[2][NB];
+  const int nkb = h / K::KB;
+  K::load(xr, 0, hh, a[0]);
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) K::load(wr[nb], 0, hh, b[0][nb]);
+  for (int kb = 0; kb < nkb; kb += 2) {
+    if (kb + 1 < nkb) {
+      K::load(xr, kb + 1, hh, a[1]);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) K::load(wr[nb], kb + 1, hh, b[1][nb]);
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) K::mma(a[0], b[0][nb], acc[nb]);
+    if (kb + 1 >= nkb) break;
+    if (kb + 2 < nkb) {
+      K::load(xr, kb + 2, hh, a[0]);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) K::load(wr[nb], kb + 2, hh, b[0][nb]);
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) K::mma(a[1], b[1][nb], acc[nb]);
+  }
+  const bool live = t0 + r < T_;
+  const int64_t t = t0 + r;
+  // expert id of element q of block nb held by this lane
+  auto col = [&](int nb, int q) { return 32 * nb + 8 * (q >> 2) + 4 * hh + (q & 3); };
+  if (logits && live) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        if (col(nb, q) < E) logits[t * E + col(nb, q)] = acc[nb][q];
+  }
+  uint32_t taken[NB] = {};
+  float selv[16];
+  int seli[16];
+  for (int j = 0; j < k; ++j) {
+    float bv = -INFINITY;
+    int bi = INT32_MAX;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int c = col(nb, q);
+        const bool ok = c < E && !((taken[nb] >> q) & 1u);
+        const float v = acc[nb][q];
+        if (ok && (v > bv || (v == bv && c < bi))) {
+          bv = v;
+          bi = c;
+        }
+      }
+    const float ov = __shfl_xor(bv, 32, 64);
+    const int oi = __shfl_xor(bi, 32, 64);
+    if (ov > bv || (ov == bv && oi < bi)) {
+      bv = ov;
+      bi = oi;
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        if (col(nb, q) == bi) taken[nb] |= 1u << q;
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj)
+      if (jj == j) {
+        selv[jj] = bv;
+        seli[jj] = bi;
+      }
+  }
+  if (hh == 0 && live) {
+    // renormalised softmax over the selected logits (the full softmax's
+    // denominator cancels); selv[0] is the largest
+    float e[16], sum = 0.f;
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj) {
+      e[jj] = jj < k ? __expf(selv[jj] - selv[0]) : 0.f;
+      sum += e[jj];
+    }
+    const float inv = 1.f / sum;
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj)
+      if (jj < k) {
+        idx[t * k + jj] = seli[jj];
+        gates[t * k + jj] = e[jj] * inv;
+      }
+  }
+}
+
+// Backward, one wave per token (grid-stride): dz_j = g_j (dg_j - sum g dg);
+// dX[t] (+)= sum_j dz_j Wr[i_j]; the dense row D[t, 0..EP) = dz scattered to
+// the selected experts (bf16 or fp32, zero elsewhere) for the weight-gradient
+// GEMM.
+template <typename T>
+__global__ __launch_bounds__(256) void router_bwd_dx_kernel(
+    const T* __restrict__ Wr, const int32_t* __restrict__ idx, const float* __restrict__ gates,
+    const float* __restrict__ dgates, int64_t T_, int h, int E, int k, int EP, int accumulate,
+    T* __restrict__ dX, T* __restrict__ D) {
+  constexpr int V = Elem<T>::kVec;  // elements per 16-byte vector
+  const int lane = threadIdx.x & 63;
+  const int64_t waves = (int64_t)gridDim.x * 4;
+  for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < T_; t += waves) {
+    float g[16], d[16], dz[16];
+    int id[16];
+    float c = 0.f;  // sum_j g_j dg_j
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      // a slot whose id lies outside [0, E) is dropped (no gradient)
+      const int i = j < k ? idx[t * k + j] : -1;
+      const bool in = i >= 0 && i < E;
+      g[j] = in ? gates[t * k + j] : 0.f;
+      d[j] = in ? dgates[t * k + j] : 0.f;
+      id[j] = in ? i : -1;
+      c = fmaf(g[j], d[j], c);
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) dz[j] = g[j] * (d[j] - c);
+    for (int c0 = lane * V; c0 < h; c0 += 64 * V) {
+      float acc[V];
+      if (accumulate) {
+        unpack16(*(const u32x4_t*)(dX + t * h + c0), acc, (T*)nullptr);
+      } else {
+#pragma unroll
+        for (int q = 0; q < V; ++q) acc[q] = 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        if (j >= k) break;
+        if (id[j] < 0) continue;
+        float w[V];
+        unpack16(*(const u32x4_t*)(Wr + (int64_t)id[j] * h + c0), w, (T*)nullptr);
+#pragma unroll
+        for (int q = 0; q < V; ++q) acc[q] = fmaf(dz[j], w[q], acc[q]);
+      }
+      *(u32x4_t*)(dX + t * h + c0) = pack16(acc, (T*)nullptr);
+    }
+    for (int e0 = lane * V; e0 < EP; e0 += 64 * V) {
+      float v[V];
+#pragma unroll
+      for (int q = 0; q < V; ++q) {
+        float s = 0.f;
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          if (j < k && id[j] == e0 + q) s += dz[j];
+        v[q] = s;
+      }
+      *(u32x4_t*)(D + t * EP + e0) = pack16(v, (T*)nullptr);
+    }
+  }
+}
+
+// dWr[e, n] (+)= sum over splits s of P[s, e, n], e < E (fixed order).
+__global__ __launch_bounds__(256) void router_reduce_kernel(const float* __restrict__ P, int S,
+                                                            int EP, int E, int h, int accumulate,
+                                                            float* __restrict__ dWr) {
+  const int64_t n4 = (int64_t)E * h / 4;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n4) return;
+  const int64_t el = i * 4;
+  const int e = (int)(el / h), n = (int)(el % h);
+  f32x4_t acc = accumulate ? *(const f32x4_t*)(dWr + el) : (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < S; ++s) acc += *(const f32x4_t*)(P + ((int64_t)s * EP + e) * h + n);
+  *(f32x4_t*)(dWr + el) = acc;
+}
+
+__global__ void iota_kernel(int32_t* p, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = i;
+}
+__global__ void split_offsets_kernel(int32_t* offsets, int32_t* order, int64_t T_, int S) {
+  const int s = blockIdx.x * 256 + threadIdx.x;
+  if (s <= S) offsets[s] = (int32_t)(s * T_ / S);
+  if (s < S) order[s] = s;
+}
+
+}  // namespace
+
+hipError_t launch_router_fwd(int dtype, const void* X, const void* Wr, int64_t T, int h, int E,
+                             int k, int32_t* idx, float* gates, float* logits, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const int blocks = (int)((T + 32 * kRouterWaves - 1) / (32 * kRouterWaves));
+  const dim3 grid(blocks), block(64 * kRouterWaves);
+  if (dtype == 0) {
+    if (E <= 32)
+      router_fwd_kernel<bf16_t, 1><<<grid, block, 0, s>>>((const bf16_t*)X, (const bf16_t*)Wr, T, h, E, k, idx, gates, logits);
+    else
+      router_fwd_kernel<bf16_t, 2><<<grid, block, 0, s>>>((const bf16_t*)X, (const bf16_t*)Wr, T, h, E, k, idx, gates, logits);
+  } else {
+    if (E <= 32)
+      router_fwd_kernel<float, 1><<<grid, block, 0, s>>>((const float*)X, (const float*)Wr, T, h, E, k, idx, gates, logits);
+    else
+      router_fwd_kernel<float, 2><<<grid, block, 0, s>>>((const float*)X, (const float*)Wr, T, h, E, k, idx, gates, logits);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_router_bwd_dx(int dtype, const void* Wr, const int32_t* idx, const float* gates,
+                                const float* dgates, int64_t T, int h, int E, int k, int EP,
+                                int accumulate, void* dX, void* D, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const int64_t want = (T + 3) / 4;
+  const int blocks = (int)(want < 8192 ? want : 8192);
+  if (dtype == 0)
+    router_bwd_dx_kernel<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t*)Wr, idx, gates, dgates, T, h, E, k, EP, accumulate, (bf16_t*)dX, (bf16_t*)D);
+  else
+    router_bwd_dx_kernel<float><<<blocks, 256, 0, s>>>((const float*)Wr, idx, gates, dgates, T, h, E, k, EP, accumulate, (float*)dX, (float*)D);
+  return hipGetLastError();
+}
+
+hipError_t launch_router_split_meta(int32_t* offsets, int32_t* order, int32_t* tok, int64_t T, int S,
+                                    hipStream_t s) {
+  split_offsets_kernel<<<(S + 1 + 255) / 256, 256, 0, s>>>(offsets, order, T, S);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || T == 0) return e;
+  iota_kernel<<<(int)((T + 255) / 256), 256, 0, s>>>(tok, (int)T);
+  return hipGetLastError();
+}
+
+hipError_t launch_router_reduce(const float* P, int S, int EP, int E, int h, int accumulate,
+                                float* dWr, hipStream_t s) {
+  const int64_t n4 = (int64_t)E * h / 4;
+  if (n4 == 0) return hipSuccess;
+  router_reduce_kernel<<<(int)((n4 + 255) / 256), 256, 0, s>>>(P, S, EP, E, h, accumulate, dWr);
+  return hipGetLastError();
+}
+
+}  // namespace memfine

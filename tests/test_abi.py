@@ -171,3 +171,22 @@ def test_binding_checks_tensor_shapes():
         mf.memfine_moe_fwd(s, 1, X, torch.zeros(16, 2, dtype=torch.int32),
                            torch.zeros(16, 2), torch.zeros(4, 128, 64, dtype=torch.bfloat16),
                            torch.zeros(4, 64, 64, dtype=torch.bfloat16), X)
+
+
+def test_router_limits_and_null_pointers_rejected_on_host():
+    L = _lib.lib()
+    fake = ctypes.c_void_p(0x1000)
+    ok = mf.make_shape(16, 64, 64, 8, 2, mf.BF16)
+    for bad in (mf.make_shape(16, 64, 64, 65, 2, mf.BF16),    # E > 64
+                mf.make_shape(16, 64, 64, 32, 17, mf.BF16),   # k > 16
+                mf.make_shape(16, 64, 64, 3, 4, mf.BF16)):    # k > E
+        assert L.memfine_router_fwd(ctypes.byref(bad), fake, fake, fake, fake, None, None) == -2
+        assert L.memfine_router_bwd(ctypes.byref(bad), *([fake] * 7), 0, 0, None, None) == -2
+    assert L.memfine_router_fwd(ctypes.byref(ok), None, fake, fake, fake, None, None) == -1
+    assert L.memfine_router_fwd(ctypes.byref(ok), fake, fake, fake, None, None, None) == -1
+    args = [fake] * 7
+    args[5] = None   # dX
+    assert L.memfine_router_bwd(ctypes.byref(ok), *args, 0, 0, None, None) == -1
+    assert L.memfine_router_bwd(ctypes.byref(ok), *([fake] * 7), 2, 0, None, None) == -1
+    assert L.memfine_router_bwd(ctypes.byref(ok), *([fake] * 7), 0, -1, None, None) == -1
+    assert L.memfine_router_fwd(None, fake, fake, fake, fake, None, None) == -1
