@@ -200,7 +200,7 @@ int tile_override() {
     const char* e = getenv("MEMFINE_TILE");
     if (!e) return 0;
     const int t = atoi(e);
-    return t == 128 ? 1 : t == 256 ? 2 : (t >= 1 && t <= 9) ? t : 0;
+    return t == 128 ? 1 : t == 256 ? 2 : (t >= 1 && t <= 11) ? t : 0;
   }();
   return v;
 }

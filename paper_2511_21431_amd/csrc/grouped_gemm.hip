@@ -56,12 +56,14 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
 
 // Tile shape: BM x BN output per workgroup of WM x WN waves, S LDS stages of
-// KB bytes of K per operand row.  DIRECT: operand tiles go from HBM straight
-// into LDS (buffer_load ... lds); else through registers (buffer_load into
-// VGPRs during the multiply of the previous tile, then ds_write_b128).
-template <int BM_, int BN_, int WM_, int WN_, int S_, int KB_ = 128, int DIRECT_ = 1> struct Cfg {
+// KB bytes of K per operand row.  DIRECT_ bit 0 (operand A) and bit 1
+// (operand B): the operand's tiles go from HBM straight into LDS
+// (buffer_load ... lds); else through registers (buffer_load into VGPRs
+// during the multiply of the previous tile, then ds_write_b128).
+template <int BM_, int BN_, int WM_, int WN_, int S_, int KB_ = 128, int DIRECT_ = 3> struct Cfg {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, S = S_, KB = KB_;
-  static constexpr bool DIRECT = DIRECT_ != 0;
+  static constexpr bool DA = (DIRECT_ & 1) != 0, DB = (DIRECT_ & 2) != 0;
+  static constexpr bool DIRECT = DA && DB;  // both direct: the deeper-stage loop
   static constexpr int NW = WM * WN, kThreads = 64 * NW;
   static constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
   static constexpr int MB = WTM / 32, NB = WTN / 32;  // 32x32 MFMA blocks per wave
@@ -473,8 +475,8 @@ __device__ __forceinline__ void store_rows(const Accum<C>& acc, T* out, int ld, 
 template <typename T, class C, bool kBwd> struct ProbFC1 {
   typedef ProbFC1 ProbSelf;
   static constexpr int kHalf = C::WTN / 2;
-  typedef KcOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
-  typedef KcOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
+  typedef KcOp<T, C::BM, C::NW, C::KB, C::DA> OA;
+  typedef KcOp<T, C::BN, C::NW, C::KB, C::DB> OB;
   OA A;
   OB B;
   static int grid(const GemmArgs& g) {
@@ -615,8 +617,8 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
 // Forward FC2: y[m, n] = sum_f a[m, f] W2[e, n, f].     K = F
 template <typename T, class C> struct ProbFC2 {
   typedef ProbFC2 ProbSelf;
-  typedef KcOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
-  typedef KcOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
+  typedef KcOp<T, C::BM, C::NW, C::KB, C::DA> OA;
+  typedef KcOp<T, C::BN, C::NW, C::KB, C::DB> OB;
   OA A;
   OB B;
   static int grid(const GemmArgs& g) {
@@ -661,8 +663,8 @@ template <typename T, class C> struct ProbFC2 {
 // (written to `ag`; the SwiGLU backward happens in the FC1 recomputation).
 template <typename T, class C> struct ProbFC2Dgrad {
   typedef ProbFC2Dgrad ProbSelf;
-  typedef KcOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
-  typedef KsOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
+  typedef KcOp<T, C::BM, C::NW, C::KB, C::DA> OA;
+  typedef KsOp<T, C::BN, C::NW, C::KB, C::DB> OB;
   OA A;
   OB B;
   uint32_t b_ktile;  // bytes of W2 per K tile (BK rows)
@@ -714,8 +716,8 @@ template <typename T, class C> struct ProbFC2Dgrad {
 // Backward FC1 dgrad: dxp[m, n] = sum_c du[m, c] W1[e, c, n].    K = 2F
 template <typename T, class C> struct ProbFC1Dgrad {
   typedef ProbFC1Dgrad ProbSelf;
-  typedef KcOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
-  typedef KsOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
+  typedef KcOp<T, C::BM, C::NW, C::KB, C::DA> OA;
+  typedef KsOp<T, C::BN, C::NW, C::KB, C::DB> OB;
   OA A;
   OB B;
   uint32_t b_ktile;
@@ -771,8 +773,8 @@ template <typename T, class C> struct ProbFC1Dgrad {
 // table, one tile ahead.  Tiles (rank, mt, nt) visit experts in descending
 // row count.
 template <typename T, class C, bool kFC1> struct ProbWgrad {
-  typedef KsOp<T, C::BM, C::NW, C::KB, C::DIRECT> OA;
-  typedef KsOp<T, C::BN, C::NW, C::KB, C::DIRECT> OB;
+  typedef KsOp<T, C::BM, C::NW, C::KB, C::DA> OA;
+  typedef KsOp<T, C::BN, C::NW, C::KB, C::DB> OB;
   static constexpr int IG = kFC1 ? OB::I : OA::I;  // copy instructions of the gathered operand
   OA A;
   OB B;
@@ -1114,6 +1116,8 @@ inline double rounds(int tiles, int per_cu) {
 
 using Big8 = Cfg<256, 256, 2, 4, 2>;        // 8 waves of 128 x 64
 using Big8R = Cfg<256, 256, 2, 4, 2, 128, 0>;  // Big8 with register-staged copies
+using Big8RA = Cfg<256, 256, 2, 4, 2, 128, 2>; // A staged, B direct
+using Big8RB = Cfg<256, 256, 2, 4, 2, 128, 1>; // A direct, B staged
 using BigR = Cfg<256, 256, 2, 2, 2, 128, 0>;   // Big with register-staged copies
 using Quarter8 = Cfg<128, 128, 4, 2, 2>;        // quarter tiles of Big8 (8 waves of 32 x 64)
 using Quarter8R = Cfg<128, 128, 4, 2, 2, 128, 0>;
@@ -1179,6 +1183,8 @@ hipError_t launch_auto(const GemmArgs& g, hipStream_t s) {
     case 7: return launch_cfg<PT, SmallS3>(g, s);
     case 8: return launch_cfg<PT, Big8R>(g, s);
     case 9: return launch_cfg<PT, BigR>(g, s);
+    case 10: return launch_cfg<PT, Big8RA>(g, s);
+    case 11: return launch_cfg<PT, Big8RB>(g, s);
     default: break;
   }
   if (PT<float, Big8>::grid(g) >= 128) {
