@@ -181,7 +181,10 @@ template <typename T, int ROWS, int NW, int KB, bool DIRECT> struct KcOp {
     for (int i = 0; i < I; ++i) {
       const int row = row_of(i, wave, lane);
       const uint32_t rb = row_byte(row);
-      voff[i] = rb == kOOB ? kOOB : rb + (uint32_t)((((lane % U) ^ kc_sw<KB>(row)) << 4));
+      // direct copies land at lane * 16, so the swizzle picks the global unit;
+      // staged copies fetch the row's units in order and swizzle on the write
+      const int unit = DIRECT ? ((lane % U) ^ kc_sw<KB>(row)) : lane % U;
+      voff[i] = rb == kOOB ? kOOB : rb + (uint32_t)(unit << 4);
     }
   }
   __device__ __forceinline__ void issue(char* lds, int kt, int wave) {
@@ -191,11 +194,12 @@ template <typename T, int ROWS, int NW, int KB, bool DIRECT> struct KcOp {
       else stage[i] = load_reg16(rs, voff[i], kt * KB);
     }
   }
-  // register-staged copy: write the K tile to LDS where the direct copy would
+  // register-staged copy: unit lane % U of the row goes to its swizzled place
   __device__ __forceinline__ void commit(char* lds, int wave, int lane) const {
     if constexpr (!DIRECT) {
 #pragma clang loop unroll(full)
-      for (int i = 0; i < I; ++i) *(u32x4_t*)(lds + (i * NW + wave) * 1024 + lane * 16) = stage[i];
+      for (int i = 0; i < I; ++i)
+        *(u32x4_t*)(lds + kc_off<KB>(row_of(i, wave, lane), lane % U)) = stage[i];
     }
   }
   __device__ __forceinline__ static typename Mma<T>::Frag read(const char* lds, int row0, int kk,
@@ -230,10 +234,12 @@ template <typename T, int ROWS, int NW, int KB, bool DIRECT> struct KsOp {
   __device__ __forceinline__ static int k_of(int i, int wave, int lane) {
     return (i * NW + wave) * KPI + (lane * 16) / P;
   }
+  // logical element column fetched by the lane (direct copies swizzle here,
+  // staged copies on the LDS write)
   __device__ __forceinline__ static int col_of(int i, int wave, int lane) {
     const int k = k_of(i, wave, lane);
     const int p = ((lane * 16) % P) >> 4;
-    return (p ^ ks_sw(k)) * V;
+    return (DIRECT ? (p ^ ks_sw(k)) : p) * V;
   }
   __device__ __forceinline__ void issue(char* lds, uint32_t soff, int wave) {
 #pragma clang loop unroll(full)
@@ -244,8 +250,12 @@ template <typename T, int ROWS, int NW, int KB, bool DIRECT> struct KsOp {
   }
   __device__ __forceinline__ void commit(char* lds, int wave, int lane) const {
     if constexpr (!DIRECT) {
+      const int p = ((lane * 16) % P) >> 4;
 #pragma clang loop unroll(full)
-      for (int i = 0; i < I; ++i) *(u32x4_t*)(lds + (i * NW + wave) * 1024 + lane * 16) = stage[i];
+      for (int i = 0; i < I; ++i) {
+        const int k = k_of(i, wave, lane);
+        *(u32x4_t*)(lds + k * P + ((p ^ ks_sw(k)) << 4)) = stage[i];
+      }
     }
   }
   __device__ __forceinline__ static int phys(int k, int col) {  // byte of element col in k-row
