@@ -9,6 +9,8 @@
 //             the FC2 backward kernel leaves for row(t,j).
 // Each thread moves one 16-byte vector of a row; consecutive threads take
 // consecutive vectors, so every row is read and written with full coalescing.
+// A token's slots are taken 8 at a time: their row ids first, then all their
+// vector loads, so the loads of one group are in flight together.
 #include "common.h"
 #include "kernels.h"
 
@@ -29,15 +31,27 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
   float acc[V];
 #pragma unroll
   for (int q = 0; q < V; ++q) acc[q] = 0.f;
-  for (int j = 0; j < k; ++j) {
-    const int r = row_of_slot[(int64_t)i * k + j];
-    if (r < 0) continue;  // dropped slot
-    const float g = gates[t * k + j];
-    const u32x4_t v = *(const u32x4_t*)(y + (int64_t)r * h + c * V);
-    float f[V];
-    unpack16(v, f, (T*)nullptr);
+  for (int j0 = 0; j0 < k; j0 += 8) {
+    int r[8];
+    float g[8];
+    u32x4_t v[8];
 #pragma unroll
-    for (int q = 0; q < V; ++q) acc[q] = fmaf(g, f[q], acc[q]);
+    for (int j = 0; j < 8; ++j) {
+      const bool in = j0 + j < k;
+      r[j] = in ? row_of_slot[(int64_t)i * k + j0 + j] : -1;
+      g[j] = in ? gates[t * k + j0 + j] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)  // dropped slots (r < 0) read row 0 with weight 0
+      v[j] = *(const u32x4_t*)(y + (int64_t)(r[j] < 0 ? 0 : r[j]) * h + c * V);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (r[j] < 0) continue;
+      float f[V];
+      unpack16(v[j], f, (T*)nullptr);
+#pragma unroll
+      for (int q = 0; q < V; ++q) acc[q] = fmaf(g[j], f[q], acc[q]);
+    }
   }
   *(u32x4_t*)(Y + t * h + c * V) = pack16(acc, (T*)nullptr);
 }
@@ -55,14 +69,22 @@ __global__ __launch_bounds__(256) void unpermute_kernel(const T* __restrict__ dx
   float acc[V];
 #pragma unroll
   for (int q = 0; q < V; ++q) acc[q] = 0.f;
-  for (int j = 0; j < k; ++j) {
-    const int r = row_of_slot[(int64_t)i * k + j];
-    if (r < 0) continue;  // dropped slot
-    const u32x4_t v = *(const u32x4_t*)(dxp + (int64_t)r * h + c * V);
-    float f[V];
-    unpack16(v, f, (T*)nullptr);
+  for (int j0 = 0; j0 < k; j0 += 8) {
+    int r[8];
+    u32x4_t v[8];
 #pragma unroll
-    for (int q = 0; q < V; ++q) acc[q] += f[q];
+    for (int j = 0; j < 8; ++j) r[j] = j0 + j < k ? row_of_slot[(int64_t)i * k + j0 + j] : -1;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)  // dropped slots (r < 0) read row 0 and are skipped
+      v[j] = *(const u32x4_t*)(dxp + (int64_t)(r[j] < 0 ? 0 : r[j]) * h + c * V);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (r[j] < 0) continue;
+      float f[V];
+      unpack16(v[j], f, (T*)nullptr);
+#pragma unroll
+      for (int q = 0; q < V; ++q) acc[q] += f[q];
+    }
   }
   *(u32x4_t*)(dX + (t0 + i) * h + c * V) = pack16(acc, (T*)nullptr);
 }
@@ -76,9 +98,13 @@ __global__ __launch_bounds__(256) void dgate_kernel(const float* __restrict__ dg
   if (i >= nslots) return;
   const int r = row_of_slot[i];
   float s = 0.f;
-  if (r >= 0) {
-    const float* p = dgp + (int64_t)r * P;
-    for (int q = 0; q < P; ++q) s += p[q];
+  if (r >= 0) {  // P = F / 32 is even: 8-byte loads, summed in index order
+    const f32x2_t* p = (const f32x2_t*)(dgp + (int64_t)r * P);
+    for (int q = 0; q < P / 2; ++q) {
+      const f32x2_t v = p[q];
+      s += v[0];
+      s += v[1];
+    }
   }
   dgates[slot0 + i] = s;
 }

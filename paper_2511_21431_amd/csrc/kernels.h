@@ -6,11 +6,18 @@
 
 namespace memfine {
 
-// Slots handled by one workgroup of the dispatch histogram / scatter kernels.
-constexpr int kDispatchSlotsPerBlock = 2048;
-
+// Slots handled by one workgroup of the dispatch histogram / scatter kernels:
+// 256 (one round of the scatter) while that needs at most 4096 workgroups,
+// else the smallest power-of-two multiple that does, which bounds the
+// per-workgroup count tables at E * 4096 entries.
+inline int dispatch_slots_per_block(int64_t n) {
+  int64_t spb = 256;
+  while ((n + spb - 1) / spb > 4096) spb *= 2;
+  return (int)spb;
+}
 inline int dispatch_blocks(int64_t n) {
-  return (int)((n + kDispatchSlotsPerBlock - 1) / kDispatchSlotsPerBlock);
+  const int spb = dispatch_slots_per_block(n);
+  return (int)((n + spb - 1) / spb);
 }
 
 // Per-chunk routing metadata produced by the dispatch kernels; all device.

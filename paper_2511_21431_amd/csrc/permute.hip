@@ -39,13 +39,13 @@ __global__ __launch_bounds__(256) void count_kernel(const int32_t* __restrict__ 
 
 // bcount[e * nb + b] = #slots of expert e in workgroup b's slot range.
 __global__ __launch_bounds__(256) void block_hist_kernel(const int32_t* __restrict__ idx, int n,
-                                                         int E, int nb,
+                                                         int E, int nb, int spb,
                                                          int32_t* __restrict__ bcount) {
   extern __shared__ int32_t hist[];
   for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
   __syncthreads();
-  const int s0 = blockIdx.x * kDispatchSlotsPerBlock;
-  const int s1 = min(n, s0 + kDispatchSlotsPerBlock);
+  const int s0 = blockIdx.x * spb;
+  const int s1 = min(n, s0 + spb);
   for (int s = s0 + threadIdx.x; s < s1; s += blockDim.x) {
     const int e = idx[s];
     if ((unsigned)e < (unsigned)E) atomicAdd(&hist[e], 1);  // ids outside [0,E) are dropped
@@ -109,14 +109,16 @@ __global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ 
 }
 
 // Stable scatter (an id outside [0, E) - which memfine_count reports - is
-// dropped: it gets no row and row_of_slot = -1).  Workgroup b walks its slot range in rounds of 256 slots
-// (4 waves x 64 lanes, in slot order).  A lane's output row is
+// dropped: it gets no row and row_of_slot = -1).  Workgroup b walks its slot
+// range in rounds of 256 slots (4 waves x 64 lanes, in slot order; with 256
+// slots per workgroup that is one round, so a chunk's slots spread over
+// n / 256 workgroups).  A lane's output row is
 //   first row of (expert, b) + slots of that expert in earlier rounds
 //   + slots of that expert in earlier waves of this round + its rank among
 //   the lanes of its own wave holding the same expert.
 __global__ __launch_bounds__(256) void scatter_kernel(
     const int32_t* __restrict__ idx, const float* __restrict__ gates, int n, int E, int k,
-    int slot0, int nb, const int32_t* __restrict__ bstart, int32_t* __restrict__ sorted_slot,
+    int slot0, int nb, int spb, const int32_t* __restrict__ bstart, int32_t* __restrict__ sorted_slot,
     int32_t* __restrict__ row_of_slot, int32_t* __restrict__ tok_of_row,
     float* __restrict__ gate_of_row) {
   extern __shared__ int32_t sh[];
@@ -127,8 +129,8 @@ __global__ __launch_bounds__(256) void scatter_kernel(
   for (int i = tid; i < 4 * E; i += 256) wc[i] = 0;
   __syncthreads();
   const int nbits = E > 1 ? 32 - __clz(E - 1) : 0;
-  const int s0 = blockIdx.x * kDispatchSlotsPerBlock;
-  const int s1 = min(n, s0 + kDispatchSlotsPerBlock);
+  const int s0 = blockIdx.x * spb;
+  const int s1 = min(n, s0 + spb);
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   for (int base = s0; base < s1; base += 256) {
     const int s = base + tid;
@@ -180,10 +182,10 @@ hipError_t launch_count(const int32_t* idx, int64_t nslots, int E, int32_t* work
 
 hipError_t launch_dispatch(const int32_t* idx, const float* gates, int64_t slot0, int n, int E,
                            int k, const ChunkMeta& m, hipStream_t s) {
-  const int nb = dispatch_blocks(n);
+  const int nb = dispatch_blocks(n), spb = dispatch_slots_per_block(n);
   const int32_t* cidx = idx + slot0;
   if (nb > 0) {
-    block_hist_kernel<<<nb, 256, E * sizeof(int32_t), s>>>(cidx, n, E, nb, m.bcount);
+    block_hist_kernel<<<nb, 256, E * sizeof(int32_t), s>>>(cidx, n, E, nb, spb, m.bcount);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
   }
@@ -191,7 +193,8 @@ hipError_t launch_dispatch(const int32_t* idx, const float* gates, int64_t slot0
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || nb == 0) return err;
   scatter_kernel<<<nb, 256, 5 * E * sizeof(int32_t), s>>>(
-      cidx, gates ? gates + slot0 : nullptr, n, E, k, (int)slot0, nb, m.bstart, m.sorted_slot, m.row_of_slot,
+      cidx, gates ? gates + slot0 : nullptr, n, E, k, (int)slot0, nb, spb, m.bstart, m.sorted_slot,
+      m.row_of_slot,
       m.tok_of_row, m.gate_of_row);
   return hipGetLastError();
 }
