@@ -573,7 +573,9 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
 
 // ------------------------------------------------------------------ router
 namespace {
-constexpr int kRouterEP = 128;  // dense dz row width fed to the split-K wgrad
+// Width of the dense dz rows fed to the split-K weight gradient: E rounded
+// up to 32 (the GEMM's M; the partials it writes scale with it).
+int router_ep(int E) { return (E + 31) / 32 * 32; }
 
 int check_router(const memfine_shape* shape) {
   int rc = check_shape(shape);
@@ -616,15 +618,16 @@ int memfine_router_bwd(const memfine_shape* shape, const void* d_X, const void* 
   }
   if (!d_X || !d_idx || !d_gates || !d_dgates || !d_dX) return MEMFINE_ERR_INVALID_ARG;
   const int64_t es = elem_bytes(S), T = S.T;
+  const int EP = router_ep(S.E);
   // split-K: enough row ranges for about 256 workgroups, each at least 256 rows
   const int ntn = (S.h + 255) / 256;
   const int64_t want = (256 + ntn - 1) / ntn, most = std::max<int64_t>(1, T / 256);
   const int splits = (int)std::max<int64_t>(1, std::min(want, most));
-  const int64_t o_meta = align256(T * kRouterEP * es);
+  const int64_t o_meta = align256(T * EP * es);
   const int64_t o_order = o_meta + align256((splits + 1) * 4);
   const int64_t o_tok = o_order + align256(splits * 4);
   const int64_t o_part = o_tok + align256(T * 4);
-  const int64_t total = o_part + align256((int64_t)splits * kRouterEP * S.h * 4);
+  const int64_t total = o_part + align256((int64_t)splits * EP * S.h * 4);
   char* ws = (char*)ws_alloc(alloc, (size_t)total, s);
   if (!ws) return MEMFINE_ERR_OOM;
   void* D = ws;
@@ -636,20 +639,20 @@ int memfine_router_bwd(const memfine_shape* shape, const void* d_X, const void* 
   hipError_t err;
   {
     KernelTimer kt(MEMFINE_K_ROUTER_BWD_DX, s, 2.0 * Td * S.k * hd,
-                   (double)es * (Td * hd * (accumulate_dX ? 2.0 : 1.0) + Td * kRouterEP) + 12.0 * Td * S.k);
+                   (double)es * (Td * hd * (accumulate_dX ? 2.0 : 1.0) + Td * EP) + 12.0 * Td * S.k);
     err = launch_router_bwd_dx(S.dtype, d_Wr, d_idx, d_gates, d_dgates, T, S.h, S.E, S.k,
-                               kRouterEP, accumulate_dX, d_dX, D, s);
+                               EP, accumulate_dX, d_dX, D, s);
   }
   if (err == hipSuccess) err = launch_router_split_meta(offsets, order, tok, T, splits, s);
   if (err == hipSuccess) {
     // dWr partials: the grouped weight-gradient GEMM over `splits` row ranges
-    // of dz^T X (M = kRouterEP rows of the dense dz, N = h, K = the range)
+    // of dz^T X (M = EP rows of the dense dz, N = h, K = the range)
     GemmArgs g = {};
     g.dtype = S.dtype;
     g.n = (int)T;
     g.E = splits;
     g.h = S.h;
-    g.F = kRouterEP / 2;
+    g.F = EP / 2;
     g.offsets = offsets;
     g.order = order;
     g.tok_of_row = tok;
@@ -659,14 +662,14 @@ int memfine_router_bwd(const memfine_shape* shape, const void* d_X, const void* 
     g.accumulate = 0;
     g.T_h_bytes = T * (int64_t)S.h * es;
     g.cus = device_cus();
-    KernelTimer kt(MEMFINE_K_ROUTER_WGRAD, s, 2.0 * Td * kRouterEP * hd,
-                   (double)es * (Td * hd + Td * kRouterEP) + 4.0 * splits * kRouterEP * hd);
+    KernelTimer kt(MEMFINE_K_ROUTER_WGRAD, s, 2.0 * Td * EP * hd,
+                   (double)es * (Td * hd + Td * EP) + 4.0 * splits * EP * hd);
     err = launch_fc1_wgrad(g, s);
   }
   if (err == hipSuccess) {
     KernelTimer kt(MEMFINE_K_ROUTER_REDUCE, s, 0.0,
                    4.0 * (double)S.E * hd * (splits + (accumulate_dWr ? 2.0 : 1.0)));
-    err = launch_router_reduce(part, splits, kRouterEP, S.E, S.h, accumulate_dWr, d_dWr, s);
+    err = launch_router_reduce(part, splits, EP, S.E, S.h, accumulate_dWr, d_dWr, s);
   }
   ws_release(alloc, ws, (size_t)total, s);
   return hip_status(err);

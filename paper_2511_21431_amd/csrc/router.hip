@@ -10,7 +10,7 @@
 namespace memfine {
 namespace {
 
-constexpr int kRouterWaves = 4;   // 32 tokens per wave, 128 per workgroup
+constexpr int kRouterWaves = 4;   // one 32-token block per workgroup, K split over the waves
 
 // Per-lane K layout of one K block.  Lane l (row l % 32, half l / 32) holds a
 // contiguous half of its row's block: for bf16 the block is 64 elements and
@@ -50,9 +50,10 @@ template <> struct RK<float> {
   }
 };
 
-// Forward.  Each wave owns 32 tokens x 32 NB experts (NB = 1 or 2); the
-// operands are loaded straight into registers one K block ahead.  After the
-// K loop lane l holds, for token l % 32, the logits of experts
+// Forward.  A workgroup owns 32 tokens x 32 NB experts (NB = 1 or 2); its
+// four waves take interleaved K blocks (wave w: blocks w, w + 4, ...) with the
+// operands loaded straight into registers one block ahead, and wave 0 sums
+// the four partial products through LDS.  After that lane l of wave 0 holds, for token l % 32, the logits of experts
 // 32 nb + 8 (q / 4) + 4 (l / 32) + q % 4 (q = 0..15); lane l ^ 32 holds the
 // token's other half.  Top-k: k rounds, each lane proposes its largest
 // unselected logit (equal: lower id), the two halves compare over one
@@ -62,10 +63,10 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_fwd_kernel(
     const T* __restrict__ X, const T* __restrict__ Wr, int64_t T_, int h, int E, int k,
     int32_t* __restrict__ idx, float* __restrict__ gates, float* __restrict__ logits) {
   typedef RK<T> K;
+  __shared__ f32x16_t part[kRouterWaves - 1][NB][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r = lane & 31, hh = lane >> 5;
-  const int64_t t0 = ((int64_t)blockIdx.x * kRouterWaves + w) * 32;
-  if (t0 >= T_) return;
+  const int64_t t0 = (int64_t)blockIdx.x * 32;
   const int64_t trow = min(t0 + r, T_ - 1);  // rows past T read the last row
   const T* xr = X + trow * h;
   const T* wr[NB];
@@ -78,26 +79,41 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_fwd_kernel(
     for (int q = 0; q < 16; ++q) acc[nb][q] = 0.f;
   typename K::Raw a[2], b[2][NB];
   const int nkb = h / K::KB;
-  K::load(xr, 0, hh, a[0]);
+  constexpr int W = kRouterWaves;
+  // this wave's K blocks: w, w + W, w + 2W, ...
+  if (w < nkb) {
+    K::load(xr, w, hh, a[0]);
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) K::load(wr[nb], 0, hh, b[0][nb]);
-  for (int kb = 0; kb < nkb; kb += 2) {
-    if (kb + 1 < nkb) {
-      K::load(xr, kb + 1, hh, a[1]);
+    for (int nb = 0; nb < NB; ++nb) K::load(wr[nb], w, hh, b[0][nb]);
+  }
+  for (int kb = w; kb < nkb; kb += 2 * W) {
+    if (kb + W < nkb) {
+      K::load(xr, kb + W, hh, a[1]);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) K::load(wr[nb], kb + 1, hh, b[1][nb]);
+      for (int nb = 0; nb < NB; ++nb) K::load(wr[nb], kb + W, hh, b[1][nb]);
     }
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) K::mma(a[0], b[0][nb], acc[nb]);
-    if (kb + 1 >= nkb) break;
-    if (kb + 2 < nkb) {
-      K::load(xr, kb + 2, hh, a[0]);
+    if (kb + W >= nkb) break;
+    if (kb + 2 * W < nkb) {
+      K::load(xr, kb + 2 * W, hh, a[0]);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) K::load(wr[nb], kb + 2, hh, b[0][nb]);
+      for (int nb = 0; nb < NB; ++nb) K::load(wr[nb], kb + 2 * W, hh, b[0][nb]);
     }
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) K::mma(a[1], b[1][nb], acc[nb]);
   }
+  // partial products of waves 1..W-1 to LDS, summed by wave 0 in wave order
+  if (w > 0) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) part[w - 1][nb][lane] = acc[nb];
+  }
+  __syncthreads();
+  if (w > 0) return;
+#pragma unroll
+  for (int ww = 0; ww < W - 1; ++ww)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[nb] += part[ww][nb][lane];
   const bool live = t0 + r < T_;
   const int64_t t = t0 + r;
   // expert id of element q of block nb held by this lane
@@ -167,60 +183,84 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_fwd_kernel(
 // Backward, one wave per token (grid-stride): dz_j = g_j (dg_j - sum g dg);
 // dX[t] (+)= sum_j dz_j Wr[i_j]; the dense row D[t, 0..EP) = dz scattered to
 // the selected experts (bf16 or fp32, zero elsewhere) for the weight-gradient
-// GEMM.
+// GEMM.  Lane j < k loads slot j and the k values are broadcast by shuffles;
+// each lane then covers NV vectors of the row per pass with their loads
+// issued together.
 template <typename T>
 __global__ __launch_bounds__(256) void router_bwd_dx_kernel(
     const T* __restrict__ Wr, const int32_t* __restrict__ idx, const float* __restrict__ gates,
     const float* __restrict__ dgates, int64_t T_, int h, int E, int k, int EP, int accumulate,
     T* __restrict__ dX, T* __restrict__ D) {
   constexpr int V = Elem<T>::kVec;  // elements per 16-byte vector
+  constexpr int NV = 4;             // vectors per lane per pass
   const int lane = threadIdx.x & 63;
   const int64_t waves = (int64_t)gridDim.x * 4;
   for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < T_; t += waves) {
-    float g[16], d[16], dz[16];
-    int id[16];
-    float c = 0.f;  // sum_j g_j dg_j
+    // slot `lane` (lanes < k); a slot whose id lies outside [0, E) is dropped
+    const int i = lane < k ? idx[t * k + lane] : -1;
+    const bool in = i >= 0 && i < E;
+    const float g = in ? gates[t * k + lane] : 0.f, d = in ? dgates[t * k + lane] : 0.f;
+    float c = g * d;  // sum over the k <= 16 slots held by lanes 0..15
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) c += __shfl_xor(c, o, 64);
+    c = __shfl(c, 0, 64);
+    const float dz = g * (d - c);
+    const int id = in ? i : -1;
+    // broadcast the k slots while every lane is active (the row loops below
+    // leave lanes idle when h or EP is short)
+    float dzs[16];
+    int ids[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      // a slot whose id lies outside [0, E) is dropped (no gradient)
-      const int i = j < k ? idx[t * k + j] : -1;
-      const bool in = i >= 0 && i < E;
-      g[j] = in ? gates[t * k + j] : 0.f;
-      d[j] = in ? dgates[t * k + j] : 0.f;
-      id[j] = in ? i : -1;
-      c = fmaf(g[j], d[j], c);
+      dzs[j] = __shfl(dz, j, 64);
+      ids[j] = j < k ? __shfl(id, j, 64) : -1;
     }
+    for (int c0 = lane * V; c0 < h; c0 += 64 * V * NV) {
+      float acc[NV][V];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) dz[j] = g[j] * (d[j] - c);
-    for (int c0 = lane * V; c0 < h; c0 += 64 * V) {
-      float acc[V];
-      if (accumulate) {
-        unpack16(*(const u32x4_t*)(dX + t * h + c0), acc, (T*)nullptr);
-      } else {
+      for (int v = 0; v < NV; ++v) {
+        const int cc = c0 + v * 64 * V;
+        if (accumulate && cc < h) {
+          unpack16(*(const u32x4_t*)(dX + t * h + cc), acc[v], (T*)nullptr);
+        } else {
 #pragma unroll
-        for (int q = 0; q < V; ++q) acc[q] = 0.f;
+          for (int q = 0; q < V; ++q) acc[v][q] = 0.f;
+        }
       }
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        if (j >= k) break;
-        if (id[j] < 0) continue;
-        float w[V];
-        unpack16(*(const u32x4_t*)(Wr + (int64_t)id[j] * h + c0), w, (T*)nullptr);
+        const float dzj = dzs[j];
+        const int idj = ids[j];
+        if (idj < 0) continue;
+        u32x4_t wv[NV];
 #pragma unroll
-        for (int q = 0; q < V; ++q) acc[q] = fmaf(dz[j], w[q], acc[q]);
+        for (int v = 0; v < NV; ++v) {
+          const int cc = c0 + v * 64 * V;
+          wv[v] = *(const u32x4_t*)(Wr + (int64_t)idj * h + (cc < h ? cc : 0));
+        }
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          float w[V];
+          unpack16(wv[v], w, (T*)nullptr);
+#pragma unroll
+          for (int q = 0; q < V; ++q) acc[v][q] = fmaf(dzj, w[q], acc[v][q]);
+        }
       }
-      *(u32x4_t*)(dX + t * h + c0) = pack16(acc, (T*)nullptr);
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int cc = c0 + v * 64 * V;
+        if (cc < h) *(u32x4_t*)(dX + t * h + cc) = pack16(acc[v], (T*)nullptr);
+      }
     }
     for (int e0 = lane * V; e0 < EP; e0 += 64 * V) {
       float v[V];
 #pragma unroll
-      for (int q = 0; q < V; ++q) {
-        float s = 0.f;
+      for (int q = 0; q < V; ++q) v[q] = 0.f;
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if (j < k && id[j] == e0 + q) s += dz[j];
-        v[q] = s;
-      }
+      for (int j = 0; j < 16; ++j)
+#pragma unroll
+        for (int q = 0; q < V; ++q)
+          if (ids[j] == e0 + q) v[q] += dzs[j];
       *(u32x4_t*)(D + t * EP + e0) = pack16(v, (T*)nullptr);
     }
   }
@@ -236,7 +276,20 @@ __global__ __launch_bounds__(256) void router_reduce_kernel(const float* __restr
   const int64_t el = i * 4;
   const int e = (int)(el / h), n = (int)(el % h);
   f32x4_t acc = accumulate ? *(const f32x4_t*)(dWr + el) : (f32x4_t){0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < S; ++s) acc += *(const f32x4_t*)(P + ((int64_t)s * EP + e) * h + n);
+  const float* p = P + (int64_t)e * h + n;
+  const int64_t stride = (int64_t)EP * h;
+  int s = 0;
+  for (; s + 4 <= S; s += 4) {  // four loads in flight, summed in split order
+    const f32x4_t v0 = *(const f32x4_t*)(p + (s + 0) * stride);
+    const f32x4_t v1 = *(const f32x4_t*)(p + (s + 1) * stride);
+    const f32x4_t v2 = *(const f32x4_t*)(p + (s + 2) * stride);
+    const f32x4_t v3 = *(const f32x4_t*)(p + (s + 3) * stride);
+    acc += v0;
+    acc += v1;
+    acc += v2;
+    acc += v3;
+  }
+  for (; s < S; ++s) acc += *(const f32x4_t*)(p + s * stride);
   *(f32x4_t*)(dWr + el) = acc;
 }
 
@@ -255,7 +308,7 @@ __global__ void split_offsets_kernel(int32_t* offsets, int32_t* order, int64_t T
 hipError_t launch_router_fwd(int dtype, const void* X, const void* Wr, int64_t T, int h, int E,
                              int k, int32_t* idx, float* gates, float* logits, hipStream_t s) {
   if (T == 0) return hipSuccess;
-  const int blocks = (int)((T + 32 * kRouterWaves - 1) / (32 * kRouterWaves));
+  const int blocks = (int)((T + 31) / 32);
   const dim3 grid(blocks), block(64 * kRouterWaves);
   if (dtype == 0) {
     if (E <= 32)
