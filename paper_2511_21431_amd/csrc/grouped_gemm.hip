@@ -500,6 +500,9 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
   __device__ __forceinline__ bool locate_sub(const GemmArgs& g, Tile& t, int b, int sub) const {
     return locate_row_subtile<ProbSelf, C::BM, BNU>(g, t, b, sub);
   }
+  __device__ __forceinline__ static int total_tiles(const GemmArgs& g) {
+    return row_tiles<C::BM>(g.offsets, g.E) * ((ncols(g) + BNU - 1) / BNU);
+  }
   __host__ __device__ static int reduction(const GemmArgs& g) { return g.h; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
     A.rs = make_rsrc(g.X, g.T_h_bytes);
@@ -642,6 +645,9 @@ template <typename T, class C> struct ProbFC2 {
   __device__ __forceinline__ bool locate_sub(const GemmArgs& g, Tile& t, int b, int sub) const {
     return locate_row_subtile<ProbSelf, C::BM, BNU>(g, t, b, sub);
   }
+  __device__ __forceinline__ static int total_tiles(const GemmArgs& g) {
+    return row_tiles<C::BM>(g.offsets, g.E) * ((ncols(g) + BNU - 1) / BNU);
+  }
   __host__ __device__ static int reduction(const GemmArgs& g) { return g.F; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
     const uint32_t rowb = (uint32_t)g.F * sizeof(T);
@@ -688,6 +694,9 @@ template <typename T, class C> struct ProbFC2Dgrad {
   }
   __device__ __forceinline__ bool locate_sub(const GemmArgs& g, Tile& t, int b, int sub) const {
     return locate_row_subtile<ProbSelf, C::BM, BNU>(g, t, b, sub);
+  }
+  __device__ __forceinline__ static int total_tiles(const GemmArgs& g) {
+    return row_tiles<C::BM>(g.offsets, g.E) * ((ncols(g) + BNU - 1) / BNU);
   }
   __host__ __device__ static int reduction(const GemmArgs& g) { return g.h; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
@@ -741,6 +750,9 @@ template <typename T, class C> struct ProbFC1Dgrad {
   }
   __device__ __forceinline__ bool locate_sub(const GemmArgs& g, Tile& t, int b, int sub) const {
     return locate_row_subtile<ProbSelf, C::BM, BNU>(g, t, b, sub);
+  }
+  __device__ __forceinline__ static int total_tiles(const GemmArgs& g) {
+    return row_tiles<C::BM>(g.offsets, g.E) * ((ncols(g) + BNU - 1) / BNU);
   }
   __host__ __device__ static int reduction(const GemmArgs& g) { return 2 * g.F; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
@@ -797,6 +809,15 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
     return ((M(g) + C::BM - 1) / C::BM) * ((N(g) + C::BN - 1) / C::BN);
   }
   static int grid(const GemmArgs& g) { return g.E * tiles_per_expert(g); }
+  __device__ __forceinline__ static int total_tiles(const GemmArgs& g) {
+    return g.E * tiles_per_expert(g);
+  }
+  __device__ __forceinline__ bool expert_of(const GemmArgs& g, Tile& t, int rank) const {
+    t.e = g.order[rank];
+    t.r0 = g.offsets[t.e];
+    t.K = g.offsets[t.e + 1] - t.r0;
+    return !(t.K == 0 && g.accumulate);  // nothing to add
+  }
   __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t, int id, int n) const {
     const int mtn = (M(g) + C::BM - 1) / C::BM, ntn = (N(g) + C::BN - 1) / C::BN;
     const int per = mtn * ntn;
@@ -804,14 +825,24 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
     const int rank = id / per;
     int mt, nt;
     tile_coords(g.raster, id - rank * per, per, mtn, ntn, mt, nt);
-    t.e = g.order[rank];
-    t.r0 = g.offsets[t.e];
-    t.K = g.offsets[t.e + 1] - t.r0;
-    if (t.K == 0 && g.accumulate) return false;  // nothing to add
+    if (!expert_of(g, t, rank)) return false;
     t.m0 = mt * C::BM;
     t.n0 = nt * C::BN;
     t.mrows = min(C::BM, M(g) - t.m0);
     return true;
+  }
+  // quarter `sub` (2 x 2) of tile b of the grid with twice the tile size
+  // (row-major within an expert): the split tail of a launch
+  __device__ __forceinline__ bool locate_sub(const GemmArgs& g, Tile& t, int b, int sub) const {
+    const int mtn2 = (M(g) + 2 * C::BM - 1) / (2 * C::BM), ntn2 = (N(g) + 2 * C::BN - 1) / (2 * C::BN);
+    const int per2 = mtn2 * ntn2;
+    const int rank = b / per2, local = b - rank * per2;
+    const int mt = local / ntn2, nt = local % ntn2;
+    if (!expert_of(g, t, rank)) return false;
+    t.m0 = (2 * mt + (sub >> 1)) * C::BM;
+    t.n0 = (2 * nt + (sub & 1)) * C::BN;
+    t.mrows = min(C::BM, M(g) - t.m0);
+    return t.mrows > 0 && t.n0 < N(g);
   }
   // tokens of K tile kt's rows for this lane's copy instructions (-1: past K)
   __device__ __forceinline__ void load_tokens(const GemmArgs& g, const Tile& t, int kt, int wave,
@@ -1023,22 +1054,22 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
   run_tile<T, C, P>(g, smem, blockIdx.x, gridDim.x);
 }
 
-// Row-grouped problem with a split tail.  Tiles of configuration C fill the
+// A launch with a split tail.  Tiles of configuration C fill the
 // full rounds (floor(tiles / cus) * cus of them); when the last, partial
 // round would hold at most cus / 2 tiles, each of its tiles runs instead as
 // four quarter tiles of configuration CQ (same workgroup size), spread over
 // four times as many CUs, so the launch ends about three quarters of a
-// round earlier.  The tile count depends on the chunk's expert offsets and is
-// computed here; workgroups past the work exit at once.
+// round earlier.  A row-grouped tile count depends on the chunk's expert
+// offsets and is computed here; workgroups past the work exit at once.  (The
+// weight gradients' last round holds the experts with the fewest rows.)
 template <typename T, class C, class CQ, class P, class PQ>
 __global__ __launch_bounds__(C::kThreads, C::kMinWaves)
 __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_gemm_split_kernel(
     GemmArgs g) {
   static_assert(C::kThreads == CQ::kThreads && C::kLds >= CQ::kLds, "quarter tiles must fit");
-  static_assert(CQ::BM * 2 == C::BM && PQ::BNU * 2 == P::BNU, "quarter tiles of the same grid");
+  static_assert(CQ::BM * 2 == C::BM && CQ::BN * 2 == C::BN, "quarter tiles of the same grid");
   __shared__ __attribute__((aligned(1024))) char smem[C::kLds];
-  const int ntn = (P::ncols(g) + P::BNU - 1) / P::BNU;
-  const int tiles = row_tiles<C::BM>(g.offsets, g.E) * ntn;
+  const int tiles = P::total_tiles(g);
   const int full = tiles / g.cus * g.cus, rem = tiles - full;
   const bool split = 2 * rem <= g.cus;
   const int id = blockIdx.x;
@@ -1141,15 +1172,9 @@ template <typename T, class C> using FC1Bwd = ProbFC1<T, C, true>;
 template <typename T, class C> using FC2W = ProbWgrad<T, C, false>;
 template <typename T, class C> using FC1W = ProbWgrad<T, C, true>;
 
-// Row-grouped problems (tiles over the chunk's rows) can split their tail.
+// Problems whose launches split a short last round into quarter tiles.
 template <template <typename, class> class PT> struct RowGrouped {
   static constexpr bool value = true;
-};
-template <> struct RowGrouped<FC2W> {
-  static constexpr bool value = false;
-};
-template <> struct RowGrouped<FC1W> {
-  static constexpr bool value = false;
 };
 
 template <template <typename, class> class PT, class C, class CQ>
