@@ -83,29 +83,27 @@ __global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ 
     bstart[i] = run;
     run += bcount[i];
   }
-  // per-expert totals, then their exclusive scan
-  int32_t c = 0;
-  if (tid < E)
-    for (int b = 0; b < nb; ++b) c += bcount[(int64_t)tid * nb + b];
-  cnt[tid] = tid < E ? c : 0;
+  // expert e's rows start where its first workgroup's rows start (the scan
+  // is expert-major), so offsets and counts follow from bstart at the
+  // expert boundaries; offsets[E] is the total (ids outside [0, E) dropped)
   __syncthreads();
-  part[tid] = cnt[tid];
-  __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    const int32_t v = tid >= off ? part[tid - off] : 0;
-    __syncthreads();
-    part[tid] += v;
-    __syncthreads();
+  const int32_t total = part[1023];
+  for (int e = tid; e < E; e += 1024) {
+    const int32_t o0 = nb > 0 ? bstart[(int64_t)e * nb] : 0;
+    const int32_t o1 = e + 1 < E ? (nb > 0 ? bstart[(int64_t)(e + 1) * nb] : 0) : total;
+    offsets[e] = o0;
+    counts[e] = o1 - o0;
+    cnt[e] = o1 - o0;
   }
-  if (tid < E) {
-    counts[tid] = c;
-    offsets[tid] = part[tid] - c;
+  if (tid == 0) offsets[E] = total;
+  __syncthreads();
+  // order: experts by descending count, ties by id
+  for (int e = tid; e < E; e += 1024) {
+    const int32_t c = cnt[e];
     int rank = 0;
-    for (int e = 0; e < E; ++e) rank += (cnt[e] > c) || (cnt[e] == c && e < tid);
-    order[rank] = tid;
+    for (int e2 = 0; e2 < E; ++e2) rank += (cnt[e2] > c) || (cnt[e2] == c && e2 < e);
+    order[rank] = e;
   }
-  // rows actually grouped (= n unless some ids were out of range)
-  if (tid == E - 1) offsets[E] = part[tid];
 }
 
 // Stable scatter (an id outside [0, E) - which memfine_count reports - is
