@@ -205,13 +205,17 @@ int tile_override() {
   return v;
 }
 
-// MEMFINE_RASTER selects the GEMM tile traversal (0..3; default 0: row-major,
-// which measured at least as fast as the XCD-grouped orders).
+// MEMFINE_RASTER selects the GEMM tile traversal for every GEMM (0..4; 0
+// row-major by workgroup id, 1..3 XCD blocks with groups of 4, 8, 16
+// m-tiles, 4 XCD blocks row-major).  Unset (-1), each problem takes its own
+// measured best: XCD blocks for the row-grouped GEMMs, the round-robin
+// expert order for the weight gradients.
+constexpr int kDefaultRaster = -1;
 int raster_mode() {
   static const int v = [] {
     const char* e = getenv("MEMFINE_RASTER");
-    const int t = e ? atoi(e) : 0;
-    return (t >= 0 && t <= 3) ? t : 0;
+    const int t = e ? atoi(e) : kDefaultRaster;
+    return (t >= -1 && t <= 4) ? t : kDefaultRaster;
   }();
   return v;
 }

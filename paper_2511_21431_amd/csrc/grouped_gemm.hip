@@ -75,17 +75,24 @@ template <int BM_, int BN_, int WM_, int WN_, int S_, int KB_ = 128, int DIRECT_
 using Big = Cfg<256, 256, 2, 2, 2>;
 using Small = Cfg<128, 128, 2, 2, 2>;
 
-// Output tiles of one XCD's resident workgroups should share operand tiles
-// in that XCD's L2.  Workgroup ids are dealt round-robin to the 8 XCDs, so
-// XCD x runs ids x, x + 8, ...; give those ids a contiguous logical range,
-// and walk the logical range in groups of kGroupM m-tiles (all n-tiles of the
-// group before the next group), so that resident workgroups cover a compact
-// block of m-tiles x n-tiles.
-__device__ __forceinline__ int xcd_remap(int id, int n) {
+// Tile order.  Workgroup ids are dealt round-robin to the 8 XCDs (XCD x
+// runs ids x, x + 8, ...), and the workgroups an XCD holds at once share its
+// L2.  Operand K-slices that several resident tiles read are then fetched
+// from memory once; tiles spread over all XCDs instead read the same slices
+// into every XCD's L2, and the copies wait on the Infinity Fabric.  So for
+// raster > 0 workgroup ids map to logical tiles in blocks of 32 consecutive
+// tiles per XCD (one workgroup per CU, 32 CUs per XCD): block b goes to XCD
+// b % 8.  Alternating blocks between XCDs keeps their loads even where tile
+// costs drift along the order (weight gradients walk the experts in
+// descending row count).  Ids past the last whole round of 256 keep their
+// index.  The map is a bijection of [0, n).
+__device__ __forceinline__ int xcd_block_remap(int id, int n) {
+  if (id >= (n & ~255)) return id;
   const int x = id & 7, slot = id >> 3;
-  const int q = n >> 3, r = n & 7;
-  return x * q + min(x, r) + slot;
+  return ((slot >> 5) << 8) | (x << 5) | (slot & 31);
 }
+// Groups of `group` m-tiles, m fastest inside a group; all n-tiles of a group
+// before the next group.  A bijection of [0, mtn * ntn) onto the grid.
 __device__ __forceinline__ void grouped_coords(int logical, int mtn, int ntn, int group, int& mt,
                                                int& nt) {
   const int per_group = group * ntn;
@@ -96,16 +103,19 @@ __device__ __forceinline__ void grouped_coords(int logical, int mtn, int ntn, in
   mt = first_m + r % gsz;
   nt = r / gsz;
 }
-// Tile coordinates of workgroup `id` of `n` on an mtn x ntn grid.  raster:
-// 0 = row-major (n-tiles fastest), else XCD-grouped with group size
-// 4 << (raster - 1) m-tiles.
-__device__ __forceinline__ void tile_coords(int raster, int id, int n, int mtn, int ntn, int& mt,
-                                            int& nt) {
-  if (raster == 0) {
-    mt = id / ntn;
-    nt = id % ntn;
+// Logical tile of workgroup `id` among the n workgroups that share the grid.
+__device__ __forceinline__ int logical_of(int raster, int id, int n) {
+  return raster <= 0 ? id : xcd_block_remap(id, n);
+}
+// Coordinates of logical tile L on an mtn x ntn grid: raster 0 and 4
+// row-major (n-tiles fastest), 1..3 groups of 4 << (raster - 1) m-tiles.
+__device__ __forceinline__ void logical_coords(int raster, int L, int mtn, int ntn, int& mt,
+                                               int& nt) {
+  if (raster >= 1 && raster <= 3) {
+    grouped_coords(L, mtn, ntn, 4 << (raster - 1), mt, nt);
   } else {
-    grouped_coords(xcd_remap(id, n), mtn, ntn, 4 << (raster - 1), mt, nt);
+    mt = L / ntn;
+    nt = L % ntn;
   }
 }
 
@@ -387,10 +397,64 @@ inline int row_tiles_bound(int n, int E, int BM) {
   return (int)(((int64_t)n + (int64_t)E * (BM - 1)) / BM);
 }
 
+// A chunk's m-tiles of BM rows, expert after expert.  With at most 64
+// experts one wave holds the whole table: lane e loads expert e's row range
+// and a shuffle scan gives the inclusive prefix of the m-tile counts, so
+// counting and locating tiles costs one load latency instead of a serial walk
+// over the experts.  All lanes of the wave must call these together.
+template <int BM> struct RowTiles {
+  int o0 = 0, o1 = 0, n = 0, inc = 0, total = 0;
+  __device__ __forceinline__ void load(const int32_t* __restrict__ offsets, int E) {
+    const int lane = threadIdx.x & 63;
+    if (lane < E) {
+      o0 = offsets[lane];
+      o1 = offsets[lane + 1];
+    }
+    n = (o1 - o0 + BM - 1) / BM;
+    inc = n;
+#pragma clang loop unroll(full)
+    for (int d = 1; d < 64; d <<= 1) {
+      const int v = __shfl_up(inc, d, 64);
+      if (lane >= d) inc += v;
+    }
+    total = __builtin_amdgcn_readlane(inc, 63);
+  }
+  // expert and rows of m-tile mt; false past the last tile.  The results are
+  // read into scalar registers (readlane): the buffer resources built from
+  // them must be wave-uniform, or every copy becomes a waterfall loop.
+  __device__ __forceinline__ bool locate(int mt, Tile& t) const {
+    const unsigned long long m = __ballot(inc > mt);
+    if (m == 0) return false;
+    const int l = __builtin_ctzll(m);  // first expert whose tiles reach past mt
+    const int before = __builtin_amdgcn_readlane(inc - n, l);
+    t.e = l;
+    t.m0 = __builtin_amdgcn_readlane(o0, l) + (mt - before) * BM;
+    t.mrows = min(BM, __builtin_amdgcn_readlane(o1, l) - t.m0);
+    return true;
+  }
+};
+
+// m-tiles of a row-grouped grid: sum_e ceil(c_e / BM).
+template <int BM> __device__ __forceinline__ int row_tiles(const int32_t* __restrict__ offsets, int E) {
+  if (E <= 64) {
+    RowTiles<BM> rt;
+    rt.load(offsets, E);
+    return rt.total;
+  }
+  int n = 0;
+  for (int e = 0; e < E; ++e) n += (offsets[e + 1] - offsets[e] + BM - 1) / BM;
+  return n;
+}
+
 // Expert and rows of m-tile `mt` of a row-grouped problem.
 template <int BM>
 __device__ __forceinline__ bool locate_rows(const int32_t* __restrict__ offsets, int E, int mt,
                                             Tile& t) {
+  if (E <= 64) {
+    RowTiles<BM> rt;
+    rt.load(offsets, E);
+    return rt.locate(mt, t);
+  }
   int acc = 0;
   for (int e = 0; e < E; ++e) {
     const int r0 = offsets[e], r1 = offsets[e + 1];
@@ -407,24 +471,44 @@ __device__ __forceinline__ bool locate_rows(const int32_t* __restrict__ offsets,
 }
 
 // Row-grouped problems: output tiles of BM rows x BNU columns (P::ncols(g)
-// columns in all), reduction length P::reduction(g).
+// columns in all), reduction length P::reduction(g).  Logical tile L of the
+// chunk's grid of row_tiles x ntn tiles; false past the grid.
+// m-tile and n-tile of logical tile L on the chunk's grid of BM-row m-tiles x
+// ntn n-tiles, with the tile's expert and rows; false past the grid.
+template <int BM>
+__device__ __forceinline__ bool locate_grid(const GemmArgs& g, int L, int ntn, Tile& t, int& nt) {
+  int mt;
+  if (g.E <= 64) {
+    RowTiles<BM> rt;
+    rt.load(g.offsets, g.E);
+    if (L >= rt.total * ntn) return false;
+    logical_coords(g.raster, L, rt.total, ntn, mt, nt);
+    return rt.locate(mt, t);
+  }
+  const int mtn = row_tiles<BM>(g.offsets, g.E);
+  if (L >= mtn * ntn) return false;
+  logical_coords(g.raster, L, mtn, ntn, mt, nt);
+  return locate_rows<BM>(g.offsets, g.E, mt, t);
+}
 template <class P, int BM, int BNU>
-__device__ __forceinline__ bool locate_row_tile(const GemmArgs& g, Tile& t, int id, int n) {
-  const int ntn = (P::ncols(g) + BNU - 1) / BNU;
-  int mt, nt;
-  tile_coords(g.raster, id, n, n / ntn, ntn, mt, nt);
-  if (!locate_rows<BM>(g.offsets, g.E, mt, t)) return false;
+__device__ __forceinline__ bool locate_row_logical(const GemmArgs& g, Tile& t, int L) {
+  int nt;
+  if (!locate_grid<BM>(g, L, (P::ncols(g) + BNU - 1) / BNU, t, nt)) return false;
   t.n0 = nt * BNU;
   t.K = P::reduction(g);
   return true;
 }
-// Quarter `sub` (2 x 2) of tile b of the grid with twice the tile size
-// (2 BM x 2 BNU, row-major order): the split tail of a launch.
+// Workgroup id of the n that share the grid.
+template <class P, int BM, int BNU>
+__device__ __forceinline__ bool locate_row_tile(const GemmArgs& g, Tile& t, int id, int n) {
+  return locate_row_logical<P, BM, BNU>(g, t, logical_of(g.raster, id, n));
+}
+// Quarter `sub` (2 x 2) of logical tile b of the grid with twice the tile
+// size: the split tail of a launch.
 template <class P, int BM, int BNU>
 __device__ __forceinline__ bool locate_row_subtile(const GemmArgs& g, Tile& t, int b, int sub) {
-  const int ntn2 = (P::ncols(g) + 2 * BNU - 1) / (2 * BNU);
-  const int mt = b / ntn2, nt = b % ntn2;
-  if (!locate_rows<2 * BM>(g.offsets, g.E, mt, t)) return false;
+  int nt;
+  if (!locate_grid<2 * BM>(g, b, (P::ncols(g) + 2 * BNU - 1) / (2 * BNU), t, nt)) return false;
   const int sm = sub >> 1, sn = sub & 1;
   t.m0 += sm * BM;
   t.mrows = min(t.mrows - sm * BM, BM);
@@ -432,13 +516,6 @@ __device__ __forceinline__ bool locate_row_subtile(const GemmArgs& g, Tile& t, i
   t.K = P::reduction(g);
   return t.mrows > 0 && t.n0 < P::ncols(g);
 }
-// Exact number of row-grouped m-tiles of BM rows: sum over experts of ceil(c_e / BM).
-template <int BM> __device__ __forceinline__ int row_tiles(const int32_t* __restrict__ offsets, int E) {
-  int n = 0;
-  for (int e = 0; e < E; ++e) n += (offsets[e + 1] - offsets[e] + BM - 1) / BM;
-  return n;
-}
-
 template <typename T> __device__ __forceinline__ const char* cptr(const void* base, int64_t el) {
   return (const char*)base + el * (int64_t)sizeof(T);
 }
@@ -484,6 +561,7 @@ __device__ __forceinline__ void store_rows(const Accum<C>& acc, T* out, int ld, 
 // Each dA element is read and then overwritten by the one lane that owns it.
 template <typename T, class C, bool kBwd> struct ProbFC1 {
   typedef ProbFC1 ProbSelf;
+  static constexpr int kRaster = 4;  // preferred tile order (XCD blocks, row-major)
   static constexpr int kHalf = C::WTN / 2;
   typedef KcOp<T, C::BM, C::NW, C::KB, C::DA> OA;
   typedef KcOp<T, C::BN, C::NW, C::KB, C::DB> OB;
@@ -630,6 +708,7 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
 // Forward FC2: y[m, n] = sum_f a[m, f] W2[e, n, f].     K = F
 template <typename T, class C> struct ProbFC2 {
   typedef ProbFC2 ProbSelf;
+  static constexpr int kRaster = 4;  // preferred tile order (XCD blocks, row-major)
   typedef KcOp<T, C::BM, C::NW, C::KB, C::DA> OA;
   typedef KcOp<T, C::BN, C::NW, C::KB, C::DB> OB;
   OA A;
@@ -679,6 +758,7 @@ template <typename T, class C> struct ProbFC2 {
 // (written to `ag`; the SwiGLU backward happens in the FC1 recomputation).
 template <typename T, class C> struct ProbFC2Dgrad {
   typedef ProbFC2Dgrad ProbSelf;
+  static constexpr int kRaster = 4;  // preferred tile order (XCD blocks, row-major)
   typedef KcOp<T, C::BM, C::NW, C::KB, C::DA> OA;
   typedef KsOp<T, C::BN, C::NW, C::KB, C::DB> OB;
   OA A;
@@ -735,6 +815,7 @@ template <typename T, class C> struct ProbFC2Dgrad {
 // Backward FC1 dgrad: dxp[m, n] = sum_c du[m, c] W1[e, c, n].    K = 2F
 template <typename T, class C> struct ProbFC1Dgrad {
   typedef ProbFC1Dgrad ProbSelf;
+  static constexpr int kRaster = 4;  // preferred tile order (XCD blocks, row-major)
   typedef KcOp<T, C::BM, C::NW, C::KB, C::DA> OA;
   typedef KsOp<T, C::BN, C::NW, C::KB, C::DB> OB;
   OA A;
@@ -795,6 +876,7 @@ template <typename T, class C> struct ProbFC1Dgrad {
 // table, one tile ahead.  Tiles (rank, mt, nt) visit experts in descending
 // row count.
 template <typename T, class C, bool kFC1> struct ProbWgrad {
+  static constexpr int kRaster = 0;  // preferred tile order: experts dealt round-robin
   typedef KsOp<T, C::BM, C::NW, C::KB, C::DA> OA;
   typedef KsOp<T, C::BN, C::NW, C::KB, C::DB> OB;
   static constexpr int IG = kFC1 ? OB::I : OA::I;  // copy instructions of the gathered operand
@@ -818,26 +900,31 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
     t.K = g.offsets[t.e + 1] - t.r0;
     return !(t.K == 0 && g.accumulate);  // nothing to add
   }
+  // logical tile L: expert rank L / per (experts in descending row count),
+  // then the tile of that expert's grid in raster order
   __device__ __forceinline__ bool locate(const GemmArgs& g, Tile& t, int id, int n) const {
     const int mtn = (M(g) + C::BM - 1) / C::BM, ntn = (N(g) + C::BN - 1) / C::BN;
     const int per = mtn * ntn;
-    // experts in descending row count; within an expert, XCD-grouped tiles
-    const int rank = id / per;
+    const int L = logical_of(g.raster, id, n);
+    const int rank = L / per;
+    if (rank >= g.E) return false;
     int mt, nt;
-    tile_coords(g.raster, id - rank * per, per, mtn, ntn, mt, nt);
+    logical_coords(g.raster, L - rank * per, mtn, ntn, mt, nt);
     if (!expert_of(g, t, rank)) return false;
     t.m0 = mt * C::BM;
     t.n0 = nt * C::BN;
     t.mrows = min(C::BM, M(g) - t.m0);
     return true;
   }
-  // quarter `sub` (2 x 2) of tile b of the grid with twice the tile size
-  // (row-major within an expert): the split tail of a launch
+  // quarter `sub` (2 x 2) of logical tile b of the grid with twice the tile
+  // size: the split tail of a launch
   __device__ __forceinline__ bool locate_sub(const GemmArgs& g, Tile& t, int b, int sub) const {
     const int mtn2 = (M(g) + 2 * C::BM - 1) / (2 * C::BM), ntn2 = (N(g) + 2 * C::BN - 1) / (2 * C::BN);
     const int per2 = mtn2 * ntn2;
-    const int rank = b / per2, local = b - rank * per2;
-    const int mt = local / ntn2, nt = local % ntn2;
+    const int rank = b / per2;
+    if (rank >= g.E) return false;
+    int mt, nt;
+    logical_coords(g.raster, b - rank * per2, mtn2, ntn2, mt, nt);
     if (!expert_of(g, t, rank)) return false;
     t.m0 = (2 * mt + (sub >> 1)) * C::BM;
     t.n0 = (2 * nt + (sub & 1)) * C::BN;
@@ -1051,7 +1138,8 @@ template <typename T, class C, class P>
 __global__ __launch_bounds__(C::kThreads, C::kMinWaves)
 __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_gemm_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(1024))) char smem[C::kLds];
-  run_tile<T, C, P>(g, smem, blockIdx.x, gridDim.x);
+  const int n = min((int)gridDim.x, P::total_tiles(g));
+  if ((int)blockIdx.x < n) run_tile<T, C, P>(g, smem, blockIdx.x, n);
 }
 
 // A launch with a split tail.  Tiles of configuration C fill the
@@ -1071,12 +1159,13 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
   __shared__ __attribute__((aligned(1024))) char smem[C::kLds];
   const int tiles = P::total_tiles(g);
   const int full = tiles / g.cus * g.cus, rem = tiles - full;
-  const bool split = 2 * rem <= g.cus;
+  const bool split = g.split_tail && 2 * rem <= g.cus;
+  const int nmain = split ? full : tiles;   // workgroups that run whole tiles
   const int id = blockIdx.x;
-  if (id < full || (!split && id < tiles)) {
+  if (id < nmain) {
     P p;
     Tile t;
-    if (p.locate(g, t, id, tiles)) run_located<T, C, P>(g, smem, p, t);
+    if (p.locate(g, t, id, nmain)) run_located<T, C, P>(g, smem, p, t);
   } else if (split && id < full + 4 * rem) {
     PQ p;
     Tile t;
@@ -1172,11 +1261,6 @@ template <typename T, class C> using FC1Bwd = ProbFC1<T, C, true>;
 template <typename T, class C> using FC2W = ProbWgrad<T, C, false>;
 template <typename T, class C> using FC1W = ProbWgrad<T, C, true>;
 
-// Problems whose launches split a short last round into quarter tiles.
-template <template <typename, class> class PT> struct RowGrouped {
-  static constexpr bool value = true;
-};
-
 template <template <typename, class> class PT, class C, class CQ>
 hipError_t launch_split_cfg(const GemmArgs& g, hipStream_t s) {
   const int bound = PT<bf16_t, C>::grid(g);
@@ -1206,7 +1290,9 @@ template <> struct StagedCopies<ProbFC1Dgrad> {
 // shape here, from 8k to 65k slots and C = 1..4; the 128 x 128 tile (two
 // workgroups per CU) only serves grids too small to give most CUs a tile.
 template <template <typename, class> class PT>
-hipError_t launch_auto(const GemmArgs& g, hipStream_t s) {
+hipError_t launch_auto(const GemmArgs& g_in, hipStream_t s) {
+  GemmArgs g = g_in;
+  if (g.raster < 0) g.raster = PT<float, Big8>::kRaster;
   if (g.dtype != 0) return launch_cfg<PT, Small>(g, s);
   switch (g.tile_override) {
     case 1: return launch_cfg<PT, Small>(g, s);
@@ -1223,20 +1309,16 @@ hipError_t launch_auto(const GemmArgs& g, hipStream_t s) {
     default: break;
   }
   if (PT<float, Big8>::grid(g) >= 128) {
-    if constexpr (RowGrouped<PT>::value) {
-      if (g.split_tail && g.raster == 0) {
-        if constexpr (StagedCopies<PT>::value) return launch_split_cfg<PT, Big8R, Quarter8R>(g, s);
-        else return launch_split_cfg<PT, Big8, Quarter8>(g, s);
-      }
-    }
-    if constexpr (StagedCopies<PT>::value) return launch_cfg<PT, Big8R>(g, s);
-    else return launch_cfg<PT, Big8>(g, s);
+    if constexpr (StagedCopies<PT>::value) return launch_split_cfg<PT, Big8R, Quarter8R>(g, s);
+    else return launch_split_cfg<PT, Big8, Quarter8>(g, s);
   }
   return launch_cfg<PT, Small>(g, s);
 }
 
 template <template <typename, class> class P1, template <typename, class> class P2>
-hipError_t launch_pair(const GemmArgs& g, hipStream_t s) {
+hipError_t launch_pair(const GemmArgs& g_in, hipStream_t s) {
+  GemmArgs g = g_in;
+  if (g.raster < 0) g.raster = 0;
   if (g.dtype == 0 && P1<float, Big8>::grid(g) + P2<float, Big8>::grid(g) < 128)
     return launch_pair_cfg<P1, P2, Small>(g, s);
   return launch_pair_cfg<P1, P2, Big8>(g, s);

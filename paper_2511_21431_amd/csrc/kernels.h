@@ -72,7 +72,7 @@ struct GemmArgs {
   int accumulate;    // wgrad: 1 = add into dW, 0 = overwrite
   int64_t T_h_bytes; // bytes of X (and of dY): T * h * element size
   int tile_override; // 0: choose the tile shape per problem; else a fixed shape
-  int raster;        // tile traversal: 0 row-major, 1..3 XCD-grouped (group 4, 8, 16)
+  int raster;        // tile order: -1 per problem; 0 row-major; 1..3 XCD blocks, groups of 4/8/16 m-tiles; 4 XCD blocks, row-major
   int cus;           // compute units of the device
   int split_tail;    // 1: row-grouped GEMMs run a short last round as quarter tiles
 };

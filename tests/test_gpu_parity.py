@@ -151,6 +151,24 @@ def test_layer_parity(mf, name, C):
         assert e <= tol, (key, e)
 
 
+@pytest.mark.parametrize("E,C", [(80, 1), (80, 3), (200, 2)])
+def test_layer_parity_many_experts(mf, E, C):
+    """More experts than one wave's lanes: the GEMMs locate their row tiles
+    by walking the experts instead of a one-wave table."""
+    w = mw.Workload(f"many-{E}", T=640, h=128, F=192, E=E, k=3, dtype="bf16", routing="dirichlet")
+    case = mw.make_case(w, 17 + E)
+    dev = device_case(w, case)
+    log(f"many experts E={E} C={C}")
+    Y = run_fwd(w, dev, C)
+    B = run_bwd(w, dev, C)
+    torch().cuda.synchronize()
+    Y_ref = om.moe_fwd(case["X"], case["idx"], case["gates"], case["W1"], case["W2"], C)
+    R = om.moe_bwd(case["X"], case["idx"], case["gates"], case["W1"], case["W2"], case["dY"], C)
+    assert relerr(host(Y), Y_ref) <= TOL["bf16"]
+    for key in ("dX", "dgates", "dW1", "dW2"):
+        assert relerr(host(B[key]), R[key]) <= TOL["bf16"], key
+
+
 @pytest.mark.parametrize("name", ["cfg1-f32", "cfg3-like", "cfg4-like"])
 def test_chunk_invariance_and_determinism(mf, name):
     w, case = small_case(name)
