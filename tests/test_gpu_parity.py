@@ -189,6 +189,21 @@ def test_chunk_invariance_and_determinism(mf, name):
                 assert relerr(B[key], ref_B[key]) < 1e-5, (C, key)
 
 
+def test_side_stream_backward_bitwise(mf, monkeypatch):
+    """The optional side-stream schedule of the backward (weight gradients
+    beside the FC1 dgrad) gives bit-identical results to the serial one."""
+    w, case = small_case("cfg2-like")
+    dev = device_case(w, case)
+    for C in (1, 3):
+        log(f"side streams C={C}")
+        monkeypatch.setenv("MEMFINE_STREAMS", "0")
+        ref = {k: host(v) for k, v in run_bwd(w, dev, C).items()}
+        monkeypatch.setenv("MEMFINE_STREAMS", "1")
+        got = {k: host(v) for k, v in run_bwd(w, dev, C).items()}
+        for key in ref:
+            assert np.array_equal(got[key], ref[key]), (C, key)
+
+
 def test_accumulate_dW(mf):
     w, case = small_case("cfg2-like")
     t = torch()
