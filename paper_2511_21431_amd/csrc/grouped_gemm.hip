@@ -1173,15 +1173,16 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
   if ((int)blockIdx.x < n) run_tile<T, C, P>(g, smem, blockIdx.x, n);
 }
 
-// Launches of direct-copy tiles of equal cost whose epilogue only stores run
-// persistent: one workgroup per CU walks ids blockIdx.x, + cus, ..., with the
-// next tile's first copies in flight during the epilogue.  The others run
+// Launches of direct-copy tiles of equal cost run persistent: one workgroup
+// per CU walks ids blockIdx.x, + cus, ..., with the next tile's first copies
+// in flight during the epilogue (after it, where the epilogue loads).  The
+// others run
 // one tile per workgroup: register-staged copies leave no registers to carry
 // a next tile, and weight-gradient tiles (K = the expert's rows) differ in
 // cost, which the hardware's dynamic dispatch balances better than a fixed
 // stride (measured 3-8 % faster).
 template <class C, class P>
-constexpr bool kPersistent = C::DIRECT && C::S == 2 && !P::kEpilogueLoads && P::kEqualTiles;
+constexpr bool kPersistent = C::DIRECT && C::S == 2 && P::kEqualTiles;
 
 // A launch with a split tail.  Tiles of configuration C fill the full
 // rounds (floor(tiles / cus) * cus of them); when the last, partial round
@@ -1218,15 +1219,24 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
       Tile tn;
       int idn = id + stride;
       bool okn = false;
-      run_located<T, C, P>(g, smem, p, t, pre, [&](char* sm, int w, int lane) {
+      // every wave at the hook or past the epilogue is past its last MFMA,
+      // so its LDS reads have returned: after a barrier the stages are free
+      auto next = [&](char* sm, int w, int lane) {
         while (idn < nmain && !(okn = pn.locate(g, tn, idn, nmain))) idn += stride;
         if (okn) {
-          // every wave is past its last MFMA, so its LDS reads have returned
           __builtin_amdgcn_s_barrier();
           pn.init(g, tn, w, lane);
           issue_prologue<T, C, P>(g, sm, pn, tn, w, lane);
         }
-      });
+      };
+      if constexpr (!P::kEpilogueLoads) {
+        run_located<T, C, P>(g, smem, p, t, pre, next);   // copies fly during the epilogue
+      } else {
+        // the epilogue's own loads would wait behind earlier copies: issue
+        // the next tile's copies once the epilogue is done
+        run_located<T, C, P>(g, smem, p, t, pre);
+        next(smem, threadIdx.x >> 6, threadIdx.x & 63);
+      }
       p = pn;
       t = tn;
       id = idn;
@@ -1392,8 +1402,12 @@ hipError_t launch_auto(const GemmArgs& g_in, hipStream_t s) {
     default: break;
   }
   if (PT<float, Big8>::grid(g) >= 128) {
-    if constexpr (StagedCopies<PT>::value) return launch_split_cfg<PT, Big8R, Quarter8R>(g, s);
-    else return launch_split_cfg<PT, Big8, Quarter8>(g, s);
+    if (g.split_tail) {
+      if constexpr (StagedCopies<PT>::value) return launch_split_cfg<PT, Big8R, Quarter8R>(g, s);
+      else return launch_split_cfg<PT, Big8, Quarter8>(g, s);
+    }
+    if constexpr (StagedCopies<PT>::value) return launch_cfg<PT, Big8R>(g, s);
+    else return launch_cfg<PT, Big8>(g, s);
   }
   return launch_cfg<PT, Small>(g, s);
 }
