@@ -193,16 +193,18 @@ ChunkBuffers carve(void* base, const Layout& L) {
   return c;
 }
 
-// MEMFINE_TILE pins the bf16 GEMM tile shape for measurements (1..7, see
-// launch_auto in grouped_gemm.hip; 128 = 1, 256 = 2).
+// Launch options for measurements and tests, read from the environment at
+// every call (a getenv per launch), so that one process can switch them.
+int env_int(const char* name, int dflt) {
+  const char* e = getenv(name);
+  return e ? atoi(e) : dflt;
+}
+
+// MEMFINE_TILE pins the bf16 GEMM tile shape (1..11, see launch_auto in
+// grouped_gemm.hip; 128 = 1, 256 = 2).
 int tile_override() {
-  static const int v = [] {
-    const char* e = getenv("MEMFINE_TILE");
-    if (!e) return 0;
-    const int t = atoi(e);
-    return t == 128 ? 1 : t == 256 ? 2 : (t >= 1 && t <= 11) ? t : 0;
-  }();
-  return v;
+  const int t = env_int("MEMFINE_TILE", 0);
+  return t == 128 ? 1 : t == 256 ? 2 : (t >= 1 && t <= 11) ? t : 0;
 }
 
 // MEMFINE_RASTER selects the GEMM tile traversal for every GEMM (0..4; 0
@@ -210,35 +212,18 @@ int tile_override() {
 // m-tiles, 4 XCD blocks row-major).  Unset (-1), each problem takes its own
 // measured best: XCD blocks for the row-grouped GEMMs, the round-robin
 // expert order for the weight gradients.
-constexpr int kDefaultRaster = -1;
 int raster_mode() {
-  static const int v = [] {
-    const char* e = getenv("MEMFINE_RASTER");
-    const int t = e ? atoi(e) : kDefaultRaster;
-    return (t >= -1 && t <= 4) ? t : kDefaultRaster;
-  }();
-  return v;
+  const int t = env_int("MEMFINE_RASTER", -1);
+  return (t >= -1 && t <= 4) ? t : -1;
 }
 
 // MEMFINE_PAIR=1 runs the FC1 dgrad and FC1 wgrad of the backward in one
 // launch (default 0: two launches).
-bool pair_launches() {
-  static const bool v = [] {
-    const char* e = getenv("MEMFINE_PAIR");
-    return e && atoi(e) == 1;
-  }();
-  return v;
-}
+bool pair_launches() { return env_int("MEMFINE_PAIR", 0) == 1; }
 
-// MEMFINE_SPLIT=0 keeps the last, partial round of a row-grouped GEMM in
-// full-size tiles (default 1: quarter tiles when it is at most half full).
-int split_tail() {
-  static const int v = [] {
-    const char* e = getenv("MEMFINE_SPLIT");
-    return (e && atoi(e) == 0) ? 0 : 1;
-  }();
-  return v;
-}
+// MEMFINE_SPLIT=0 keeps the last, partial round of a GEMM in full-size tiles
+// (default 1: quarter tiles when it is at most half full).
+int split_tail() { return env_int("MEMFINE_SPLIT", 1) == 0 ? 0 : 1; }
 
 // Compute units of the current device (cached per device id).
 int device_cus() {
@@ -263,10 +248,7 @@ int hip_status(hipError_t e) { return e == hipSuccess ? MEMFINE_OK : MEMFINE_ERR
 // the caller's stream).  Measured on MI355X: 4 % faster on the 7168-wide
 // 32-expert workload at C = 2, 1 % slower on the 2048-wide one, equal at
 // C = 1; the concurrent launches mostly split the CUs between them.
-bool overlap_streams() {  // read at every call: tests switch it per call
-  const char* e = getenv("MEMFINE_STREAMS");
-  return e && atoi(e) == 1;
-}
+bool overlap_streams() { return env_int("MEMFINE_STREAMS", 0) == 1; }
 
 // Two side streams per device (non-blocking, default priority) and the
 // events of one fork/join.  `mu` is held from the fork to the join, so that
