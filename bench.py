@@ -162,12 +162,16 @@ def main():
     # ---- timed region
     mf.memfine_profile_begin([dominant])
     torch.cuda.synchronize()
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    ends[0].record()
+    for i in range(args.steps):
         step()
+        ends[i + 1].record()   # per-step GPU time between consecutive step ends
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     prof = mf.memfine_profile_end()
+    step_ms = sorted(a.elapsed_time(b) for a, b in zip(ends, ends[1:]))
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     tokens_per_s = w.T * args.steps / (t1 - t0)
     d = prof[dominant]
@@ -239,6 +243,9 @@ def main():
                    "T": w.T, "h": w.h, "F": w.F, "E": w.E, "k": w.k,
                    "chunks": C, "budget_bytes": budget, "bins": list(bins),
                    "parallelism": "single GPU (one expert-parallel share)"},
+        "step_ms_median": round(step_ms[len(step_ms) // 2], 4),
+        "step_ms_min": round(step_ms[0], 4),
+        "slots_per_s": round(w.N * args.steps / (t1 - t0), 1),
         "mfma_util_layer": round(executed_flops / (ms_per_step * 1e-3) / 1e12 / peak, 4),
         "layer_tflops": round(executed_flops / (ms_per_step * 1e-3) / 1e12, 1),
         "roofline": {"kernel": dominant, "bound": "mfma", "achieved": round(achieved, 1),
@@ -324,6 +331,28 @@ def bench_router(mf, torch, w, shape, dev, layer_step, steps):
                     "workload's seeded routing"}
 
 
+def host_cpu():
+    """CPU model and the BLAS library NumPy calls (for the oracle's timing)."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = "unknown"
+    try:
+        from threadpoolctl import threadpool_info
+        libs = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if libs:
+            blas = f"{libs[0].get('internal_api')} {libs[0].get('version')}"
+    except Exception:
+        pass
+    return {"model": model, "blas": blas}
+
+
 def cpu_baseline(w, idx_np, gates_np, dev, C, target_s):
     """The oracle, as it stands, on the host: fp64 fwd + chunked-recompute bwd
     over the first T_s tokens (same weights, same chunk count)."""
@@ -354,7 +383,7 @@ def cpu_baseline(w, idx_np, gates_np, dev, C, target_s):
     del W1, W2
     torch.cuda.synchronize()
     return {"value": round(Ts / elapsed, 2), "unit": "tokens/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "cpu": host_cpu(),
             "sample": f"first {Ts} of {w.T} tokens, fp64 NumPy oracle fwd + chunked-recompute "
                       f"bwd at C={C}, {elapsed:.1f} s"}
 
