@@ -42,8 +42,9 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
       g[j] = in ? gates[t * k + j0 + j] : 0.f;
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j)  // dropped slots (r < 0) read row 0 with weight 0
-      v[j] = *(const u32x4_t*)(y + (int64_t)(r[j] < 0 ? 0 : r[j]) * h + c * V);
+    for (int j = 0; j < 8; ++j)  // (k is uniform: no load past the token's slots;
+      if (j0 + j < k)            // a dropped slot, r < 0, reads row 0 with weight 0)
+        v[j] = *(const u32x4_t*)(y + (int64_t)(r[j] < 0 ? 0 : r[j]) * h + c * V);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       if (r[j] < 0) continue;
@@ -75,8 +76,9 @@ __global__ __launch_bounds__(256) void unpermute_kernel(const T* __restrict__ dx
 #pragma unroll
     for (int j = 0; j < 8; ++j) r[j] = j0 + j < k ? row_of_slot[(int64_t)i * k + j0 + j] : -1;
 #pragma unroll
-    for (int j = 0; j < 8; ++j)  // dropped slots (r < 0) read row 0 and are skipped
-      v[j] = *(const u32x4_t*)(dxp + (int64_t)(r[j] < 0 ? 0 : r[j]) * h + c * V);
+    for (int j = 0; j < 8; ++j)  // (k is uniform: no load past the token's slots;
+      if (j0 + j < k)            // a dropped slot, r < 0, reads row 0 and is skipped)
+        v[j] = *(const u32x4_t*)(dxp + (int64_t)(r[j] < 0 ? 0 : r[j]) * h + c * V);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       if (r[j] < 0) continue;

@@ -7,10 +7,13 @@
 // over one expert at a time and multiplied by 32x32 MFMA instructions
 // (v_mfma_f32_32x32x16_bf16, or v_mfma_f32_32x32x2f32 on the fp32 path).
 //
-// Operand movement.  Every operand tile goes from HBM straight into LDS with
-// buffer_load ... lds (16 bytes per lane, no staging registers); buffer
-// resources bound each tensor, so rows past the end of a tensor, ragged
-// tails and the K tail of a weight-gradient tile read as zero in hardware.
+// Operand movement.  Operand tiles go from HBM into LDS either directly with
+// buffer_load ... lds (16 bytes per lane, no staging registers: forward GEMMs
+// and weight gradients) or through registers (buffer_load into VGPRs during
+// the previous K tile's multiply, then ds_write_b128: the two dgrads, where
+// that measured faster).  Buffer resources bound each tensor, so rows past
+// the end of a tensor, ragged tails and the K tail of a weight-gradient tile
+// read as zero in hardware.
 // Two LDS layouts serve the two ways an operand can sit in HBM:
 //   K-contiguous  ([row][k], 128-byte K rows): activation rows, weights used
 //                 as W^T.  Rows may be gathered through the chunk's
@@ -24,14 +27,20 @@
 // Both layouts XOR-swizzle 16-byte units so that the lanes of one LDS read
 // instruction hit distinct banks.
 //
-// Tiling.  A workgroup is 4 waves (2 x 2) and owns a BM x BN output tile;
-// each wave owns (BM/2) x (BN/2) as (BM/64) x (BN/64) MFMA blocks whose
-// accumulators stay in registers for the whole K loop.  The 256 x 256 tile
-// (128 x 128 per wave) reads each LDS operand byte into 4 MFMAs, which keeps
-// LDS and L2 traffic under the matrix cores' rate; 128 x 128 tiles serve
-// problems whose 256 x 256 grid would leave CUs idle.  K tiles (128 bytes of
-// K per operand row) are double-buffered: the copy of tile k+1 runs while
-// the waves multiply tile k, with one barrier per K step.
+// Tiling.  A workgroup of WM x WN waves owns a BM x BN output tile; each
+// wave owns (BM/WM) x (BN/WN) as 32 x 32 MFMA blocks whose accumulators stay
+// in registers for the whole K loop.  The default is 256 x 256 on 8 waves
+// (2 x 4, 128 x 64 per wave, two waves per SIMD, one workgroup per CU);
+// 128 x 128 tiles serve problems whose 256 x 256 grid would leave CUs idle
+// and the quarter-tile tail of a launch.  K tiles (128 bytes of K per
+// operand row) are double-buffered in 128 KB of LDS: the copy of tile k+1
+// runs while the waves multiply tile k, with one barrier per K step.
+//
+// Tile order.  Workgroups are dealt round-robin to the 8 XCDs; the
+// row-grouped GEMMs map ids to tiles in blocks of 32 per XCD so that the
+// tiles one XCD holds at once share operand K-slices in its L2, and launches
+// of equal-cost direct-copy tiles run persistent (one workgroup per CU, the
+// next tile's first copies in flight during the epilogue).
 //
 // Scheduling on skewed expert loads: the row-grouped GEMMs (forward FC1/FC2,
 // dgrads) enumerate m-tiles expert after expert from the chunk's offsets, so
