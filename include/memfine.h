@@ -13,9 +13,15 @@
  * ---------------------------------------
  * - Pointers named d_* are device pointers, h_* host pointers.  Every buffer
  *   is owned by the caller; the library keeps no state between calls except a
- *   lazily created per-process profiling table and, for calls made with a
- *   NULL allocator, one lazily created stream-ordered memory pool per device
- *   (its freed chunk memory is kept for reuse until the process ends).
+ *   lazily created per-process profiling table, for calls made with a NULL
+ *   allocator one lazily created stream-ordered memory pool per device (its
+ *   freed chunk memory is kept for reuse until the process ends), and, only
+ *   when MEMFINE_STREAMS=1 is set, two side streams and three events per
+ *   device (kept until the process ends).
+ * - Environment variables MEMFINE_TILE, MEMFINE_RASTER, MEMFINE_SPLIT,
+ *   MEMFINE_PAIR and MEMFINE_STREAMS, read at every call, select alternative
+ *   GEMM tile shapes, tile orders and launch schedules for measurement; every
+ *   setting gives bit-identical results.
  * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *   Device work is enqueued asynchronously on it; only memfine_count and
  *   memfine_profile_end synchronise (with the stream / the recorded events).
