@@ -344,6 +344,34 @@ def test_allocator_hook_peak_and_oom(mf):
 
 # ---------------------------------------------------- full-size, sampled
 # (5, 16): the budget sweep's largest chunk count on its 131072-token batch
+def test_full_size_workload2_every_output(mf):
+    """The benchmark's workload (T=8192, h=2048, F=1408, E=16, top-4, the
+    planner's C=2) checked in full against the oracle: every Y, dX and dgates
+    entry and every weight-gradient element (about 6 s of oracle time)."""
+    t = torch()
+    w, C = W[2], 2
+    idx, gates = mw.make_routing(w, 2)
+    dev = mw.make_tensors_device(w, 2, "cuda")
+    dev["idx"] = t.from_numpy(idx).cuda()
+    dev["gates"] = t.from_numpy(gates).cuda()
+    log("full check cfg2 C=2: fwd + bwd")
+    Y = host(run_fwd(w, dev, C))
+    B = {k: host(v) for k, v in run_bwd(w, dev, C).items()}
+    X = dev["X"].double().cpu().numpy()
+    W1 = dev["W1"].double().cpu().numpy()
+    W2 = dev["W2"].double().cpu().numpy()
+    dY = dev["dY"].double().cpu().numpy()
+    log("full check cfg2 C=2: oracle")
+    Y_ref = om.moe_fwd(X, idx, gates, W1, W2, C)
+    R = om.moe_bwd(X, idx, gates, W1, W2, dY, C)
+    errs = {"Y": relerr(Y, Y_ref)}
+    for key in ("dX", "dgates", "dW1", "dW2"):
+        errs[key] = relerr(B[key], R[key])
+    log("  cfg2 C=2 full: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    for key, e in errs.items():
+        assert e <= TOL["bf16"], (key, e)
+
+
 FULL = [(2, 2), (2, 1), (3, 4), (4, 4), (5, 16)]
 
 
