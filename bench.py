@@ -31,7 +31,6 @@ import numpy as np  # noqa: E402
 
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 PEAK_HBM_GBS = 8000.0
-HBM_GBS = 8000.0
 
 # activation budget handed to the planner per workload (bytes); the plan
 # then picks C from the bins
@@ -177,12 +176,20 @@ def main():
     d = prof[dominant]
     avg_ms = d["total_ms"] / d["launches"]
     flops_per_launch = d["flops"] / d["launches"]
-    achieved = flops_per_launch / (avg_ms * 1e-3) / 1e12
+    bytes_per_launch = d["bytes"] / d["launches"]
     peak = PEAK_TFLOPS[w.dtype]
+    # the kernel's roofline: whichever of its algorithmic flops at the MFMA
+    # peak and its algorithmic bytes at the HBM peak takes longer
+    t_mfma = flops_per_launch / (peak * 1e12)
+    t_hbm = bytes_per_launch / (PEAK_HBM_GBS * 1e9)
+    bound = "hbm" if t_hbm > t_mfma else "mfma"
+    achieved_tflops = flops_per_launch / (avg_ms * 1e-3) / 1e12
+    achieved_gbs = bytes_per_launch / (avg_ms * 1e-3) / 1e9
+    achieved = achieved_gbs if bound == "hbm" else achieved_tflops
     traffic = read_traffic(dominant, f"cfg{cfg}")
     executed_flops = 22.0 * w.N * w.h * w.F
     log(f"[bench] {ms_per_step:.3f} ms/step, {tokens_per_s:.0f} tokens/s, dominant {dominant} "
-        f"avg {avg_ms:.3f} ms {achieved:.1f} TFLOP/s")
+        f"avg {avg_ms:.3f} ms {achieved_tflops:.1f} TFLOP/s {achieved_gbs:.1f} GB/s ({bound}-bound)")
 
     # ---- chunk-count sweep: throughput and measured peak activation memory
     sweep = []
@@ -248,10 +255,15 @@ def main():
         "slots_per_s": round(w.N * args.steps / (t1 - t0), 1),
         "mfma_util_layer": round(executed_flops / (ms_per_step * 1e-3) / 1e12 / peak, 4),
         "layer_tflops": round(executed_flops / (ms_per_step * 1e-3) / 1e12, 1),
-        "roofline": {"kernel": dominant, "bound": "mfma", "achieved": round(achieved, 1),
-                     "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+        "roofline": {"kernel": dominant, "bound": bound, "achieved": round(achieved, 1),
+                     "peak": PEAK_HBM_GBS if bound == "hbm" else peak,
+                     "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
+                     "frac": round(achieved / (PEAK_HBM_GBS if bound == "hbm" else peak), 4),
                      "traffic": traffic, "avg_launch_ms": round(avg_ms, 4),
-                     "launches": d["launches"], "flops_per_launch": flops_per_launch},
+                     "launches": d["launches"], "flops_per_launch": flops_per_launch,
+                     "bytes_per_launch": bytes_per_launch,
+                     "achieved_tflops": round(achieved_tflops, 1),
+                     "achieved_gbs": round(achieved_gbs, 1)},
         "kernels_one_step": {k: {"ms": round(v["total_ms"], 4),
                                  "tflops": round(v["flops"] / max(v["total_ms"], 1e-9) / 1e9, 1),
                                  "gbs": round(v["bytes"] / max(v["total_ms"], 1e-9) / 1e6, 1)}
