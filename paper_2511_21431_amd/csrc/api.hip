@@ -75,6 +75,7 @@ struct Layout {
     kBcount, kBstart, kCounts, kOffsets, kOrder, kSorted, kRowOf, kTokOf, kGateOf,
     kA, kY,                 // forward
     kU, kAg, kDxp, kDgp,    // backward
+    kCtr,                   // backward: tile counters of the two weight gradients
     kNum
   };
   int64_t off[kNum];
@@ -105,6 +106,7 @@ void chunk_layout(const memfine_shape& s, int64_t n, int pass, Layout& L) {
     L.size[Layout::kAg] = n * s.F * es;
     L.size[Layout::kDxp] = n * s.h * es;
     L.size[Layout::kDgp] = n * P * 4;
+    L.size[Layout::kCtr] = 2 * 4;
   }
   int64_t o = 0;
   for (int i = 0; i < Layout::kNum; ++i) {
@@ -170,6 +172,7 @@ struct ChunkBuffers {
   ChunkMeta m;
   void *a, *y, *u, *ag, *dxp;
   float* dgp;
+  int32_t* ctr;  // [2] tile counters: FC1 wgrad, FC2 wgrad
 };
 
 ChunkBuffers carve(void* base, const Layout& L) {
@@ -190,6 +193,7 @@ ChunkBuffers carve(void* base, const Layout& L) {
   c.ag = b + L.off[Layout::kAg];
   c.dxp = b + L.off[Layout::kDxp];
   c.dgp = (float*)(b + L.off[Layout::kDgp]);
+  c.ctr = (int32_t*)(b + L.off[Layout::kCtr]);
   return c;
 }
 
@@ -585,11 +589,15 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
       }
       if (err == hipSuccess) {
         KernelTimer kt(MEMFINE_K_FC1_WGRAD, ss->s[0], w_fc1w.flops, w_fc1w.bytes);
-        err = launch_fc1_wgrad(g, ss->s[0]);
+        GemmArgs gw = g;
+        gw.tile_ctr = cb.ctr;
+        err = launch_fc1_wgrad(gw, ss->s[0]);
       }
       if (err == hipSuccess) {
         KernelTimer kt(MEMFINE_K_FC2_WGRAD, ss->s[1], w_fc2w.flops, w_fc2w.bytes);
-        err = launch_fc2_wgrad(g, ss->s[1]);
+        GemmArgs gw = g;
+        gw.tile_ctr = cb.ctr + 1;
+        err = launch_fc2_wgrad(gw, ss->s[1]);
       }
       if (err == hipSuccess) {
         KernelTimer kt(MEMFINE_K_FC1_DGRAD, s, w_fc1d.flops, w_fc1d.bytes);
@@ -610,7 +618,9 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
     } else {
       if (err == hipSuccess) {
         KernelTimer kt(MEMFINE_K_FC2_WGRAD, s, w_fc2w.flops, w_fc2w.bytes);
-        err = launch_fc2_wgrad(g, s);
+        GemmArgs gw = g;
+        gw.tile_ctr = cb.ctr + 1;
+        err = launch_fc2_wgrad(gw, s);
       }
       if (pair_launches()) {
         if (err == hipSuccess) {
@@ -621,7 +631,9 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
       } else {
         if (err == hipSuccess) {
           KernelTimer kt(MEMFINE_K_FC1_WGRAD, s, w_fc1w.flops, w_fc1w.bytes);
-          err = launch_fc1_wgrad(g, s);
+          GemmArgs gw = g;
+          gw.tile_ctr = cb.ctr;
+          err = launch_fc1_wgrad(gw, s);
         }
         if (err == hipSuccess) {
           KernelTimer kt(MEMFINE_K_FC1_DGRAD, s, w_fc1d.flops, w_fc1d.bytes);

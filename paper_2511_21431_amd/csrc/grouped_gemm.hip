@@ -1192,6 +1192,14 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
 // stride (measured 3-8 % faster).
 template <class C, class P>
 constexpr bool kPersistent = C::DIRECT && C::S == 2 && P::kEqualTiles;
+// Weight gradients (direct copies, tile cost = the expert's rows) run
+// persistent with a tile counter when the launch provides one: each
+// workgroup takes the next tile in launch order (experts by descending row
+// count) from the counter, fetched one tile ahead, so that CUs that finish
+// early take more tiles; the next tile's first copies fly during the
+// epilogue's dW stores.
+template <class C, class P>
+constexpr bool kDynamic = C::DIRECT && C::S == 2 && !P::kEqualTiles && !P::kEpilogueLoads;
 
 // A launch with a split tail.  Tiles of configuration C fill the full
 // rounds (floor(tiles / cus) * cus of them); when the last, partial round
@@ -1251,6 +1259,61 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
       id = idn;
       ok = okn;
       pre = okn;
+    }
+    if (split) {
+      for (int q = blockIdx.x; q < 4 * rem; q += stride) {
+        PQ pq;
+        Tile tq;
+        __syncthreads();  // the previous tile's waves are done with the stages
+        if (pq.locate_sub(g, tq, full + q / 4, q % 4)) run_located<T, CQ, PQ>(g, smem, pq, tq);
+      }
+    }
+  } else if (kDynamic<C, P> && g.tile_ctr != nullptr) {
+    __shared__ int32_t s_next;
+    // thread 0 takes a tile index; every wave reads it after a barrier (and
+    // again before thread 0 may overwrite it)
+    auto grab = [&]() {
+      if (threadIdx.x == 0) s_next = atomicAdd(g.tile_ctr, 1);
+      __syncthreads();
+      const int v = s_next;
+      __syncthreads();
+      return v;
+    };
+    P p;
+    Tile t;
+    int v = grab();
+    bool pre = false;
+    for (;;) {
+      if (!pre) {
+        while (v < nmain && !p.locate(g, t, v, nmain)) v = grab();
+        if (v >= nmain) break;
+      }
+      int32_t ahead = 0;  // thread 0: the next tile index, fetched during this tile
+      if (threadIdx.x == 0) ahead = atomicAdd(g.tile_ctr, 1);
+      P pn;
+      Tile tn;
+      int vn = nmain;
+      bool okn = false;
+      run_located<T, C, P>(g, smem, p, t, pre, [&](char* sm, int w, int lane) {
+        if (threadIdx.x == 0) s_next = ahead;
+        __syncthreads();  // s_next is visible; every wave is past its last MFMA
+        vn = s_next;
+        okn = vn < nmain && pn.locate(g, tn, vn, nmain);
+        if (okn) {
+          pn.init(g, tn, w, lane);
+          issue_prologue<T, C, P>(g, sm, pn, tn, w, lane);
+        }
+      });
+      if (okn) {
+        p = pn;
+        t = tn;
+      }
+      v = vn;
+      pre = okn;
+      // without a prefetched tile, the grab in the locate loop above (or the
+      // quarter-tile barrier below) separates this tile's LDS use from the
+      // next one's, and lets every wave read s_next before it changes
+      if (!okn) __syncthreads();
     }
     if (split) {
       for (int q = blockIdx.x; q < 4 * rem; q += stride) {
@@ -1367,7 +1430,13 @@ template <template <typename, class> class PT, class C, class CQ>
 hipError_t launch_split_cfg(const GemmArgs& g, hipStream_t s) {
   const int bound = PT<bf16_t, C>::grid(g);
   if (bound <= 0) return hipSuccess;
-  const int blocks = kPersistent<C, PT<bf16_t, C>> ? std::min(bound, g.cus) : bound + 3 * (g.cus / 2);
+  const bool dynamic = kDynamic<C, PT<bf16_t, C>> && g.tile_ctr != nullptr;
+  if (dynamic) {  // the tile counter starts at 0 for this launch
+    const hipError_t err = launch_fill_i32(g.tile_ctr, 1, 0, s);
+    if (err != hipSuccess) return err;
+  }
+  const int blocks = (kPersistent<C, PT<bf16_t, C>> || dynamic) ? std::min(bound, g.cus)
+                                                                 : bound + 3 * (g.cus / 2);
   grouped_gemm_split_kernel<bf16_t, C, CQ, PT<bf16_t, C>, PT<bf16_t, CQ>>
       <<<blocks, C::kThreads, 0, s>>>(g);
   return hipGetLastError();

@@ -75,6 +75,8 @@ struct GemmArgs {
   int raster;        // tile order: -1 per problem; 0 row-major; 1..3 XCD blocks, groups of 4/8/16 m-tiles; 4 XCD blocks, row-major
   int cus;           // compute units of the device
   int split_tail;    // 1: row-grouped GEMMs run a short last round as quarter tiles
+  int32_t* tile_ctr; // weight gradients: device tile counter (one int) for a dynamic
+                     // persistent launch, or null for one tile per workgroup
 };
 
 int dgate_partials(int F);
