@@ -80,6 +80,21 @@ template <int BM_, int BN_, int WM_, int WN_, int S_, int KB_ = 128, int DIRECT_
   static constexpr int kLds = S * kStage;
   static constexpr int kWgPerCu = (160 * 1024) / kLds;
   static constexpr int kMinWaves = (kWgPerCu * NW + 3) / 4 < 3 ? (kWgPerCu * NW + 3) / 4 : 3;
+  // Wave w's block of the tile.  Waves w and w + 4 of a workgroup share a
+  // SIMD (checked on the GPU with HW_ID).  On the 2 x 4 grid the two waves
+  // of a SIMD take different wave rows and column halves (w < 4: (0, w);
+  // w >= 4: (1, (w + 2) % 4)), so that a tile whose lower half of rows or
+  // right half of columns lies past the data still keeps every SIMD's
+  // matrix core busy with the other wave's blocks (see `active`).
+  __device__ __forceinline__ static void wave_role(int w, int& wm, int& wn) {
+    if constexpr (WM == 2 && WN == 4) {
+      wm = w >> 2;
+      wn = (w + 2 * (w >> 2)) & 3;
+    } else {
+      wm = w / WN;
+      wn = w % WN;
+    }
+  }
 };
 using Big = Cfg<256, 256, 2, 2, 2>;
 using Small = Cfg<128, 128, 2, 2, 2>;
@@ -525,6 +540,13 @@ __device__ __forceinline__ bool locate_row_subtile(const GemmArgs& g, Tile& t, i
   t.K = P::reduction(g);
   return t.mrows > 0 && t.n0 < P::ncols(g);
 }
+// Does wave (wm, wn) own any output of a row-grouped tile?  Its rows start
+// at wm * WTM and its BNU / WN output columns at n0 + wn * BNU / WN.
+template <class P, class C, int BNU>
+__device__ __forceinline__ bool row_wave_active(const GemmArgs& g, const Tile& t, int wm, int wn) {
+  return wm * C::WTM < t.mrows && t.n0 + wn * (BNU / C::WN) < P::ncols(g);
+}
+
 template <typename T> __device__ __forceinline__ const char* cptr(const void* base, int64_t el) {
   return (const char*)base + el * (int64_t)sizeof(T);
 }
@@ -591,6 +613,9 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
   }
   __device__ __forceinline__ static int total_tiles(const GemmArgs& g) {
     return row_tiles<C::BM>(g.offsets, g.E) * ((ncols(g) + BNU - 1) / BNU);
+  }
+  __device__ __forceinline__ bool active(const GemmArgs& g, const Tile& t, int wm, int wn) const {
+    return row_wave_active<ProbSelf, C, BNU>(g, t, wm, wn);
   }
   __host__ __device__ static int reduction(const GemmArgs& g) { return g.h; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
@@ -740,6 +765,9 @@ template <typename T, class C> struct ProbFC2 {
   __device__ __forceinline__ static int total_tiles(const GemmArgs& g) {
     return row_tiles<C::BM>(g.offsets, g.E) * ((ncols(g) + BNU - 1) / BNU);
   }
+  __device__ __forceinline__ bool active(const GemmArgs& g, const Tile& t, int wm, int wn) const {
+    return row_wave_active<ProbSelf, C, BNU>(g, t, wm, wn);
+  }
   __host__ __device__ static int reduction(const GemmArgs& g) { return g.F; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
     const uint32_t rowb = (uint32_t)g.F * sizeof(T);
@@ -792,6 +820,9 @@ template <typename T, class C> struct ProbFC2Dgrad {
   }
   __device__ __forceinline__ static int total_tiles(const GemmArgs& g) {
     return row_tiles<C::BM>(g.offsets, g.E) * ((ncols(g) + BNU - 1) / BNU);
+  }
+  __device__ __forceinline__ bool active(const GemmArgs& g, const Tile& t, int wm, int wn) const {
+    return row_wave_active<ProbSelf, C, BNU>(g, t, wm, wn);
   }
   __host__ __device__ static int reduction(const GemmArgs& g) { return g.h; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
@@ -851,6 +882,9 @@ template <typename T, class C> struct ProbFC1Dgrad {
   }
   __device__ __forceinline__ static int total_tiles(const GemmArgs& g) {
     return row_tiles<C::BM>(g.offsets, g.E) * ((ncols(g) + BNU - 1) / BNU);
+  }
+  __device__ __forceinline__ bool active(const GemmArgs& g, const Tile& t, int wm, int wn) const {
+    return row_wave_active<ProbSelf, C, BNU>(g, t, wm, wn);
   }
   __host__ __device__ static int reduction(const GemmArgs& g) { return 2 * g.F; }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
@@ -912,6 +946,10 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
   static int grid(const GemmArgs& g) { return g.E * tiles_per_expert(g); }
   __device__ __forceinline__ static int total_tiles(const GemmArgs& g) {
     return g.E * tiles_per_expert(g);
+  }
+  // does wave (wm, wn) own any element of the tile?
+  __device__ __forceinline__ bool active(const GemmArgs& g, const Tile& t, int wm, int wn) const {
+    return wm * C::WTM < t.mrows && t.n0 + wn * C::WTN < N(g);
   }
   __device__ __forceinline__ bool expert_of(const GemmArgs& g, Tile& t, int rank) const {
     t.e = g.order[rank];
@@ -1116,7 +1154,12 @@ __device__ __forceinline__ void issue_prologue(const GemmArgs& g, char* smem, P&
 template <typename T, class C, class P, class Next = NoNext>
 __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p, const Tile& t,
                                             bool prefetched = false, Next next = Next()) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w / C::WN, wn = w % C::WN;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int wm, wn;
+  C::wave_role(w, wm, wn);
+  // a wave whose whole block lies past the tile's rows or columns skips its
+  // fragment reads and MFMAs (its epilogue stores nothing)
+  const bool active = p.active(g, t, wm, wn);
   if (!prefetched) p.init(g, t, w, lane);
   Accum<C> acc;
   p.init_acc(g, t, acc, wm, wn, lane);
@@ -1138,7 +1181,8 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
         p.issue(g, t, kt + C::S - 1, st, st + C::BM * C::KB, w, lane);
       }
       char* cur = smem + (kt % C::S) * C::kStage;
-      mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
+      if (active)
+        mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
     }
   } else {
     // Register-staged double buffer: the loads of tile kt + 1 are in flight
@@ -1156,7 +1200,8 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
       char* nxt = smem + ((kt + 1) & 1) * C::kStage;
       const bool more = kt + 1 < nk;
       if (more) p.issue(g, t, kt + 1, nxt, nxt + C::BM * C::KB, w, lane);
-      mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
+      if (active)
+        mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
       if (more) {
         wait_vm<0>();
         p.commit(nxt, nxt + C::BM * C::KB, w, lane);
