@@ -155,6 +155,14 @@ __device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, char* lds, 
 __device__ __forceinline__ u32x4_t load_reg16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
 }
+// 16-byte store; an offset past the resource's range is dropped by the
+// hardware, so the instruction issues whatever the lane's element is
+__device__ __forceinline__ void store_f32x4(__amdgpu_buffer_rsrc_t r, uint32_t voff, const float (&v)[4]) {
+  f32x4_t x;
+#pragma clang loop unroll(full)
+  for (int c = 0; c < 4; ++c) x[c] = v[c];
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, x), r, voff, 0, 0);
+}
 
 template <typename T> struct Mma;
 template <> struct Mma<bf16_t> {
@@ -305,8 +313,14 @@ __device__ __forceinline__ int ks_phys(int k, int col) {
   const int b = col * ES;
   return k * P + ((((b >> 4) ^ ks_sw(k))) << 4) + (b & 15);
 }
+// `lds` is restrict: inlined, the transposing reads then carry alias-scope
+// information, without which the compiler makes every LDS read wait for all
+// direct-to-LDS copies in flight (those of the next K tile included, which
+// write the other stage); the K loop's own waits and barriers order the
+// copies and the reads.
 template <int ROWS>
-__device__ __forceinline__ bf16x8_t ks_read_bf16(const char* lds, int col0, int kk, int lane) {
+__device__ __forceinline__ bf16x8_t ks_read_bf16(const char* __restrict__ lds, int col0, int kk,
+                                                 int lane) {
   // MFMA lane l wants column col0 + l%32 and K values 8*(l/32) .. +7.  In the
   // 16-lane group G = l/16, source lane j supplies 4 columns starting at
   // col0 + 16*(G%2) + 4*(j%4) of k-row 16 kk + 8*(G/2) + 4h + j/4; after the
@@ -926,7 +940,9 @@ template <typename T, class C> struct ProbFC1Dgrad {
 // computes its per-lane row offsets for every K tile from the row -> token
 // table, one tile ahead.  Tiles (rank, mt, nt) visit experts in descending
 // row count.
-template <typename T, class C, bool kFC1> struct ProbWgrad {
+// kAcc: 1 adds to dW, 0 overwrites it, -1 reads which from GemmArgs (a
+// fixed mode lets the compiler drop the other path's loads and their waits).
+template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
   static constexpr int kRaster = 0;  // preferred tile order: experts dealt round-robin
   static constexpr bool kEqualTiles = false;  // K = the expert's rows
   static constexpr bool kEpilogueLoads = false;  // the epilogue reads global memory
@@ -940,6 +956,10 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
   int32_t tok[D][IG];        // gathered operand: tokens of the next D K tiles' rows
   __host__ __device__ static int M(const GemmArgs& g) { return kFC1 ? 2 * g.F : g.h; }
   __host__ __device__ static int N(const GemmArgs& g) { return kFC1 ? g.h : g.F; }
+  __device__ __forceinline__ static bool acc_on(const GemmArgs& g) {
+    return kAcc < 0 ? g.accumulate != 0 : kAcc == 1;
+  }
+  static constexpr bool kAccLoads = kAcc != 0;
   __host__ __device__ static int tiles_per_expert(const GemmArgs& g) {
     return ((M(g) + C::BM - 1) / C::BM) * ((N(g) + C::BN - 1) / C::BN);
   }
@@ -955,7 +975,7 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
     t.e = g.order[rank];
     t.r0 = g.offsets[t.e];
     t.K = g.offsets[t.e + 1] - t.r0;
-    return !(t.K == 0 && g.accumulate);  // nothing to add
+    return !(t.K == 0 && acc_on(g));  // nothing to add
   }
   // logical tile L: expert rank L / per (experts in descending row count),
   // then the tile of that expert's grid in raster order
@@ -988,15 +1008,27 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
     t.mrows = min(C::BM, M(g) - t.m0);
     return t.mrows > 0 && t.n0 < N(g);
   }
-  // tokens of K tile kt's rows for this lane's copy instructions (-1: past K)
+  // row k (within the expert) of this lane's copy instruction i in K tile kt
+  __device__ __forceinline__ static int k_row(int kt, int i, int wave, int lane) {
+    return kt * OA::BKE + (kFC1 ? OB::k_of(i, wave, lane) : OA::k_of(i, wave, lane));
+  }
+  // Tokens of K tile kt's rows for this lane's copy instructions.  Buffer
+  // loads over the expert's rows: the lane's offset is fixed and the K tile
+  // goes in the scalar offset, so no address register is rewritten in the K
+  // loop (a fragment read reusing one while a load still reads it would have
+  // to wait for the load and, vector-memory instructions retiring in order,
+  // for every copy in flight); rows past K read as 0 and are masked when the
+  // copies are issued.  The values are not touched here, for the same
+  // reason.
   __device__ __forceinline__ void load_tokens(const GemmArgs& g, const Tile& t, int kt, int wave,
                                               int lane, int32_t (&dst)[IG]) {
+    const int r0 = __builtin_amdgcn_readfirstlane(t.r0);
+    const int K = __builtin_amdgcn_readfirstlane(t.K);
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(g.tok_of_row + r0, (int64_t)max(K, 0) * 4);
 #pragma clang loop unroll(full)
-    for (int i = 0; i < IG; ++i) {
-      const int k = kt * OA::BKE + (kFC1 ? OB::k_of(i, wave, lane) : OA::k_of(i, wave, lane));
-      const int32_t v = g.tok_of_row[t.r0 + min(k, t.K - 1)];
-      dst[i] = k < t.K ? v : -1;
-    }
+    for (int i = 0; i < IG; ++i)
+      dst[i] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(
+          rs, (uint32_t)k_row(0, i, wave, lane) * 4, (uint32_t)kt * OA::BKE * 4, 0);
   }
   // the non-gathered operand (rows r0 .. r0+K of u for FC1, of ag for FC2) is
   // re-based at every K tile, so its offsets stay small for any row count
@@ -1049,7 +1081,7 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
   // from clamped in-range addresses; those accumulators are never stored.
   __device__ __forceinline__ void init_acc(const GemmArgs& g, const Tile& t, Accum<C>& acc, int wm,
                                           int wn, int lane) const {
-    if (!g.accumulate) {
+    if (!acc_on(g)) {
       zero_acc(acc);
       return;
     }
@@ -1074,13 +1106,22 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
     A.commit(As, wave, lane);
     B.commit(Bs, wave, lane);
   }
-  __device__ __forceinline__ void issue(const GemmArgs& g, const Tile& t, int kt, char* As,
-                                        char* Bs, int wave, int lane) {
+  // byte offsets of the gathered operand's copies of K tile kt (tokens in tok[0])
+  __device__ __forceinline__ void gather_offsets(const GemmArgs& g, const Tile& t, int kt, int wave,
+                                                 int lane, uint32_t (&gv)[IG]) const {
     const uint32_t rowb = (uint32_t)g.h * sizeof(T);
-    uint32_t* gv = kFC1 ? B.voff : A.voff;
+    // branch-free: a row past K or a column past the operand gets bit 31
+    // (kOOB), which puts the offset past the resource (a byte of X or dY is
+    // below 2^31); colb already is kOOB for such a column
 #pragma clang loop unroll(full)
     for (int i = 0; i < IG; ++i)
-      gv[i] = (tok[0][i] < 0 || colb[i] == kOOB) ? kOOB : (uint32_t)tok[0][i] * rowb + colb[i];
+      gv[i] = ((uint32_t)tok[0][i] * rowb + colb[i]) |
+              (k_row(kt, i, wave, lane) >= t.K ? kOOB : 0u);
+  }
+  __device__ __forceinline__ void issue(const GemmArgs& g, const Tile& t, int kt, char* As,
+                                        char* Bs, int wave, int lane) {
+    if constexpr (kFC1) gather_offsets(g, t, kt, wave, lane, B.voff);
+    else gather_offsets(g, t, kt, wave, lane, A.voff);
     if (kFC1) A.rs = plain_rsrc(g, t, kt);
     else B.rs = plain_rsrc(g, t, kt);
     A.issue(As, 0, wave);
@@ -1091,24 +1132,33 @@ template <typename T, class C, bool kFC1> struct ProbWgrad {
       for (int i = 0; i < IG; ++i) tok[d][i] = tok[d + 1][i];
     load_tokens(g, t, kt + D, wave, lane, tok[D - 1]);  // D tiles ahead
   }
+  // Vector-memory instructions epilogue() issues: every one, whatever the
+  // tile's extent (elements outside it get an offset past the range).
+  static constexpr int kEpiStores = C::MB * C::NB * 4;
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
                                            int wm, int wn, int lane) const {
-    float* dW = (kFC1 ? g.dW1 : g.dW2) + (int64_t)t.e * M(g) * N(g);
     const int Nn = N(g);  // % 64 == 0: a run of 4 columns is all in or all out
+    const uint32_t rowb = (uint32_t)Nn * sizeof(float);
+    // the tile is the workgroup's: its fields are uniform, which the compiler
+    // cannot always prove (the resource must sit in scalar registers)
+    const int e = __builtin_amdgcn_readfirstlane(t.e);
+    const int m0 = __builtin_amdgcn_readfirstlane(t.m0);
+    const int mrows = __builtin_amdgcn_readfirstlane(t.mrows);
+    const __amdgpu_buffer_rsrc_t rs =
+        make_rsrc((kFC1 ? g.dW1 : g.dW2) + (int64_t)e * M(g) * Nn + (int64_t)m0 * Nn,
+                  (int64_t)mrows * rowb);
 #pragma clang loop unroll(full)
     for (int mb = 0; mb < C::MB; ++mb) {
       const int r = acc_row<C>(wm, mb, lane);
-      if (r >= t.mrows) continue;
-      float* o = dW + (int64_t)(t.m0 + r) * Nn;
+      const uint32_t ro = r < mrows ? (uint32_t)r * rowb : kOOB;
 #pragma clang loop unroll(full)
       for (int nb = 0; nb < C::NB; ++nb)
 #pragma clang loop unroll(full)
         for (int gq = 0; gq < 4; ++gq) {
           const int n = t.n0 + acc_col<C>(wn, nb, gq, lane);
-          if (n >= Nn) continue;
           float v[4];
           acc_run(acc.v[mb][nb], gq, v);
-          Vec4<float>::store(o + n, v);
+          store_f32x4(rs, n < Nn ? ro + (uint32_t)n * sizeof(float) : kOOB, v);
         }
     }
   }
@@ -1130,6 +1180,19 @@ template <int N> __device__ __forceinline__ void wait_vm() {
 struct NoNext {
   __device__ __forceinline__ void operator()(char*, int, int) const {}
 };
+// Problems whose init_acc may load the accumulators (P::acc_on tells when).
+template <class P, class = void> struct AccLoads { static constexpr bool value = false; };
+template <class P> struct AccLoads<P, decltype((void)P::kAccLoads)> {
+  static constexpr bool value = P::kAccLoads;
+};
+// Problems whose epilogue issues a fixed count of vector-memory instructions
+// (P::kEpiStores) can take the deep prefetch below.
+template <class P, class = void> struct HasEpiStores { static constexpr bool value = false; };
+template <class P> struct HasEpiStores<P, decltype((void)P::kEpiStores)> {
+  static constexpr bool value = true;
+};
+template <class C, class P>
+constexpr bool kDeep = C::DIRECT && C::S == 2 && HasEpiStores<P>::value;
 // K tiles of a tile's reduction.
 template <typename T, class C> __device__ __forceinline__ int k_tiles(const Tile& t) {
   constexpr int BKE = C::KB / (int)sizeof(T);
@@ -1147,13 +1210,41 @@ __device__ __forceinline__ void issue_prologue(const GemmArgs& g, char* smem, P&
   }
 }
 
+// Copies of a located tile's first two K tiles into both stages of a
+// two-stage ring, issued before the previous tile's epilogue: its stores then
+// queue behind them and the first two K steps need not wait for the stores.
+template <typename T, class C, class P>
+__device__ __forceinline__ void issue_prologue2(const GemmArgs& g, char* smem, P& p, const Tile& t,
+                                                int w, int lane) {
+  static_assert(C::DIRECT && C::S == 2, "two-stage direct-copy ring");
+  const int nk = k_tiles<T, C>(t);
+#pragma clang loop unroll(full)
+  for (int j = 0; j < 2; ++j) {
+    char* st = smem + j * C::kStage;
+    if (j < nk) p.issue(g, t, j, st, st + C::BM * C::KB, w, lane);
+  }
+}
+// vmcnt operand for "the N most recent vector-memory instructions may still
+// be in flight"; with more than the counter holds in flight, waiting for 62
+// still retires everything older (the wave cannot have more outstanding)
+constexpr int vm_cap(int n) { return n < 62 ? n : 62; }
+
 // One output tile.  `prefetched`: the previous tile of this workgroup already
 // ran p.init and issued the copies of the first S - 1 K tiles.  `next` runs
 // after the K loop, before the epilogue (with the LDS stages free once it
 // has passed a barrier).
+//
+// `deep` (two-stage direct-copy rings of problems whose epilogue issues a
+// fixed P::kEpiStores vector-memory instructions): the previous tile issued
+// this tile's first two K tiles (issue_prologue2) and then its epilogue, so
+// at K step 0 the copies of K tile 1 and those stores, and at step 1 the
+// stores, were issued after the copies waited for.  Vector-memory
+// instructions retire in order, so waiting until only that many are in
+// flight suffices, and the stores drain under the first two K steps.
 template <typename T, class C, class P, class Next = NoNext>
 __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p, const Tile& t,
-                                            bool prefetched = false, Next next = Next()) {
+                                            bool prefetched = false, Next next = Next(),
+                                            bool deep = false) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int wm, wn;
   C::wave_role(w, wm, wn);
@@ -1163,20 +1254,33 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
   if (!prefetched) p.init(g, t, w, lane);
   Accum<C> acc;
   p.init_acc(g, t, acc, wm, wn, lane);
+  // Accumulators loaded from memory: wait here, once.  Left to the compiler,
+  // the waits for them land inside the K loop's multiply (its loop state
+  // merges this entry with the loop's own), where they also wait for the
+  // copies each K step has just issued.
+  if constexpr (AccLoads<P>::value)
+    if (p.acc_on(g)) wait_vm<0>();
   constexpr int kCopies = P::OA::I + P::OB::I;  // copy instructions per wave per K tile
   const int nk = k_tiles<T, C>(t);
   if constexpr (C::DIRECT) {
     if (!prefetched) issue_prologue<T, C, P>(g, smem, p, t, w, lane);
     for (int kt = 0; kt < nk; ++kt) {
-      if (kt + C::S - 2 < nk) wait_vm<(C::S - 2) * kCopies>();
-      else wait_vm<0>();
+      if constexpr (kDeep<C, P>) {
+        if (deep && kt == 0 && nk > 1) wait_vm<vm_cap(kCopies + P::kEpiStores)>();
+        else if (deep && kt < 2) wait_vm<vm_cap(P::kEpiStores)>();
+        else wait_vm<0>();
+      } else if (kt + C::S - 2 < nk) {
+        wait_vm<(C::S - 2) * kCopies>();
+      } else {
+        wait_vm<0>();
+      }
       // A bare s_barrier: __syncthreads() would add a memory fence, for which
       // the compiler waits for every copy in flight (vmcnt(0)) and so defeats
       // the deeper stages.  The explicit wait above already makes this wave's
       // copies of tile kt visible, and every LDS read of the stage the next
       // copy overwrites has returned (its MFMA has issued).
       __builtin_amdgcn_s_barrier();
-      if (kt + C::S - 1 < nk) {
+      if (kt + C::S - 1 < nk && !(deep && kt + C::S - 1 < 2)) {
         char* st = smem + ((kt + C::S - 1) % C::S) * C::kStage;
         p.issue(g, t, kt + C::S - 1, st, st + C::BM * C::KB, w, lane);
       }
@@ -1260,7 +1364,12 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
     GemmArgs g) {
   static_assert(C::kThreads == CQ::kThreads && C::kLds >= CQ::kLds, "quarter tiles must fit");
   static_assert(CQ::BM * 2 == C::BM && CQ::BN * 2 == C::BN, "quarter tiles of the same grid");
-  __shared__ __attribute__((aligned(1024))) char smem[C::kLds];
+  // One LDS object: the stages, then (dynamic launches) the next tile index.
+  // With a second __shared__ variable the compiler scopes every LDS access
+  // by variable and then cannot tell a fragment read of one stage from the
+  // copies into the other, so each K step's reads would wait for the next
+  // step's copies.
+  __shared__ __attribute__((aligned(1024))) char smem[C::kLds + 16];
   const int tiles = P::total_tiles(g);
   const int full = tiles / g.cus * g.cus, rem = tiles - full;
   const bool split = g.split_tail && 2 * rem <= g.cus;
@@ -1314,13 +1423,13 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
       }
     }
   } else if (kDynamic<C, P> && g.tile_ctr != nullptr) {
-    __shared__ int32_t s_next;
+    int32_t& s_next = *reinterpret_cast<int32_t*>(smem + C::kLds);
     // thread 0 takes a tile index; every wave reads it after a barrier (and
     // again before thread 0 may overwrite it)
     auto grab = [&]() {
       if (threadIdx.x == 0) s_next = atomicAdd(g.tile_ctr, 1);
       __syncthreads();
-      const int v = s_next;
+      const int v = __builtin_amdgcn_readfirstlane(s_next);  // uniform: scalar tile state
       __syncthreads();
       return v;
     };
@@ -1333,8 +1442,20 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
         while (v < nmain && !p.locate(g, t, v, nmain)) v = grab();
         if (v >= nmain) break;
       }
-      int32_t ahead = 0;  // thread 0: the next tile index, fetched during this tile
-      if (threadIdx.x == 0) ahead = atomicAdd(g.tile_ctr, 1);
+      // thread 0: the next tile index, fetched during this tile.  Left
+      // undefined for the other threads (which never read it), so that no
+      // copy of the result at the end of the branch waits for the atomic -
+      // and, vector-memory instructions retiring in order, for everything
+      // issued before it.
+      // (The offset is an opaque per-lane zero: with a provably uniform
+      // address the compiler aggregates the atomic over the wave and reads
+      // its result back at once.)
+      int32_t ahead;
+      if (threadIdx.x == 0) {
+        int32_t zero;
+        asm volatile("v_mov_b32 %0, 0" : "=v"(zero));
+        ahead = atomicAdd(g.tile_ctr + zero, 1);
+      }
       P pn;
       Tile tn;
       int vn = nmain;
@@ -1342,13 +1463,14 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
       run_located<T, C, P>(g, smem, p, t, pre, [&](char* sm, int w, int lane) {
         if (threadIdx.x == 0) s_next = ahead;
         __syncthreads();  // s_next is visible; every wave is past its last MFMA
-        vn = s_next;
+        vn = __builtin_amdgcn_readfirstlane(s_next);
         okn = vn < nmain && pn.locate(g, tn, vn, nmain);
         if (okn) {
           pn.init(g, tn, w, lane);
-          issue_prologue<T, C, P>(g, sm, pn, tn, w, lane);
+          if constexpr (kDeep<C, P>) issue_prologue2<T, C, P>(g, sm, pn, tn, w, lane);
+          else issue_prologue<T, C, P>(g, sm, pn, tn, w, lane);
         }
-      });
+      }, kDeep<C, P> && pre);
       if (okn) {
         p = pn;
         t = tn;
@@ -1470,6 +1592,10 @@ template <typename T, class C> using FC1Fwd = ProbFC1<T, C, false>;
 template <typename T, class C> using FC1Bwd = ProbFC1<T, C, true>;
 template <typename T, class C> using FC2W = ProbWgrad<T, C, false>;
 template <typename T, class C> using FC1W = ProbWgrad<T, C, true>;
+template <typename T, class C> using FC2WNew = ProbWgrad<T, C, false, 0>;
+template <typename T, class C> using FC2WAdd = ProbWgrad<T, C, false, 1>;
+template <typename T, class C> using FC1WNew = ProbWgrad<T, C, true, 0>;
+template <typename T, class C> using FC1WAdd = ProbWgrad<T, C, true, 1>;
 
 template <template <typename, class> class PT, class C, class CQ>
 hipError_t launch_split_cfg(const GemmArgs& g, hipStream_t s) {
@@ -1554,8 +1680,12 @@ hipError_t launch_fc1_recompute(const GemmArgs& g, hipStream_t s) { return launc
 hipError_t launch_fc2_fwd(const GemmArgs& g, hipStream_t s) { return launch_auto<ProbFC2>(g, s); }
 hipError_t launch_fc2_dgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<ProbFC2Dgrad>(g, s); }
 hipError_t launch_fc1_dgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<ProbFC1Dgrad>(g, s); }
-hipError_t launch_fc2_wgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<FC2W>(g, s); }
-hipError_t launch_fc1_wgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<FC1W>(g, s); }
+hipError_t launch_fc2_wgrad(const GemmArgs& g, hipStream_t s) {
+  return g.accumulate ? launch_auto<FC2WAdd>(g, s) : launch_auto<FC2WNew>(g, s);
+}
+hipError_t launch_fc1_wgrad(const GemmArgs& g, hipStream_t s) {
+  return g.accumulate ? launch_auto<FC1WAdd>(g, s) : launch_auto<FC1WNew>(g, s);
+}
 hipError_t launch_fc1_dgrad_wgrad(const GemmArgs& g, hipStream_t s) {
   return launch_pair<ProbFC1Dgrad, FC1W>(g, s);
 }
