@@ -99,6 +99,20 @@ template <int BM_, int BN_, int WM_, int WN_, int S_, int KB_ = 128, int DIRECT_
 using Big = Cfg<256, 256, 2, 2, 2>;
 using Small = Cfg<128, 128, 2, 2, 2>;
 
+// Epilogue staging.  Straight from the accumulators, a 16-byte store
+// instruction would touch 32 rows (one per lane pair) in 8- or 16-byte
+// pieces.  Bounced through a wave-private LDS slab of 32 rows x 128 bytes
+// (16-byte units XOR-swizzled by row), each instruction writes 8 rows x 128
+// contiguous bytes instead.  The slabs sit after the stages (wave w at
+// kLds + w * kSlabBytes), where the LDS has room.
+constexpr int kSlabBytes = 32 * 128;
+template <class C> constexpr int kSlabArea =
+    C::kLds + C::NW * kSlabBytes <= 160 * 1024 ? C::NW * kSlabBytes : 0;
+template <class C> __device__ __forceinline__ char* slab_of(char* smem, int wave) {
+  if constexpr (kSlabArea<C> > 0) return smem + C::kLds + wave * kSlabBytes;
+  else return nullptr;
+}
+
 // Tile order.  Workgroup ids are dealt round-robin to the 8 XCDs (XCD x
 // runs ids x, x + 8, ...), and the workgroups an XCD holds at once share its
 // L2.  Operand K-slices that several resident tiles read are then fetched
@@ -569,7 +583,55 @@ template <typename T> __device__ __forceinline__ const char* cptr(const void* ba
 // an output of `ld` columns (ld % 64 == 0).
 template <typename T, class C>
 __device__ __forceinline__ void store_rows(const Accum<C>& acc, T* out, int ld, const Tile& t, int wm,
-                                           int wn, int lane) {
+                                           int wn, int lane, char* slab = nullptr) {
+  if constexpr (sizeof(T) == 2 && (C::WTN * 2) % 128 == 0) {
+    if (slab != nullptr) {
+      // bf16 rows of the wave's block in 128-byte column groups (64 columns,
+      // two 32-column MFMA blocks); per (row block mb, group): the lanes write
+      // their runs of row lane % 32 into the slab, then read back 16 bytes
+      // each, 8 lanes to a row, and store 8 rows per instruction.  Elements
+      // outside the tile get an offset past the resource (ld % 8 == 0: a
+      // 16-byte unit is all in or all out).
+      constexpr int CG = C::WTN * 2 / 128;
+      const int m0 = __builtin_amdgcn_readfirstlane(t.m0);
+      const int mrows = __builtin_amdgcn_readfirstlane(t.mrows);
+      const int n0 = __builtin_amdgcn_readfirstlane(t.n0);
+      const uint32_t rowb = (uint32_t)ld * 2;
+      const __amdgpu_buffer_rsrc_t rs = make_rsrc(out + (int64_t)m0 * ld, (int64_t)mrows * rowb);
+      const int rr = lane & 31, half = lane >> 5;
+#pragma clang loop unroll(full)
+      for (int mb = 0; mb < C::MB; ++mb)
+#pragma clang loop unroll(full)
+        for (int cg = 0; cg < CG; ++cg) {
+#pragma clang loop unroll(full)
+          for (int b = 0; b < 2; ++b)
+#pragma clang loop unroll(full)
+            for (int gq = 0; gq < 4; ++gq) {
+              const int byte = b * 64 + gq * 16 + half * 8;  // run's byte in the 128-byte row
+              float v[4];
+              acc_run(acc.v[mb][cg * 2 + b], gq, v);
+              u32x2_t x;
+              x[0] = pack_bf16x2(v[0], v[1]);
+              x[1] = pack_bf16x2(v[2], v[3]);
+              *(u32x2_t*)(slab + rr * 128 + ((((byte >> 4) ^ (rr & 7))) << 4) + (byte & 15)) = x;
+            }
+          asm volatile("" ::: "memory");  // the writes above before the reads below
+          const int unit = lane & 7;
+#pragma clang loop unroll(full)
+          for (int q = 0; q < 4; ++q) {
+            const int r = (lane >> 3) + 8 * q;
+            const u32x4_t x = *(const u32x4_t*)(slab + r * 128 + ((unit ^ (r & 7)) << 4));
+            const int row = wm * C::WTM + mb * 32 + r;
+            const int col = n0 + wn * C::WTN + cg * 64 + unit * 8;
+            __builtin_amdgcn_raw_buffer_store_b128(
+                x, rs, (row < mrows && col < ld) ? (uint32_t)row * rowb + (uint32_t)col * 2 : kOOB, 0,
+                0);
+          }
+          asm volatile("" ::: "memory");  // the reads above before the next writes
+        }
+      return;
+    }
+  }
 #pragma clang loop unroll(full)
   for (int mb = 0; mb < C::MB; ++mb) {
     const int r = acc_row<C>(wm, mb, lane);
@@ -659,7 +721,7 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
     B.issue(Bs, kt, wave);
   }
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
-                                           int wm, int wn, int lane) const {
+                                           int wm, int wn, int lane, char* slab) const {
     if constexpr (kBwd) {
       epilogue_bwd(g, t, acc, wm, wn, lane);
     } else {
@@ -804,8 +866,8 @@ template <typename T, class C> struct ProbFC2 {
     B.issue(Bs, kt, wave);
   }
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
-                                           int wm, int wn, int lane) const {
-    store_rows<T, C>(acc, (T*)g.y, g.h, t, wm, wn, lane);
+                                           int wm, int wn, int lane, char* slab) const {
+    store_rows<T, C>(acc, (T*)g.y, g.h, t, wm, wn, lane, slab);
   }
 };
 
@@ -867,8 +929,8 @@ template <typename T, class C> struct ProbFC2Dgrad {
     B.issue(Bs, kt * b_ktile, wave);
   }
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
-                                           int wm, int wn, int lane) const {
-    store_rows<T, C>(acc, (T*)g.ag, g.F, t, wm, wn, lane);
+                                           int wm, int wn, int lane, char* slab) const {
+    store_rows<T, C>(acc, (T*)g.ag, g.F, t, wm, wn, lane, slab);
   }
 };
 
@@ -928,8 +990,8 @@ template <typename T, class C> struct ProbFC1Dgrad {
     B.issue(Bs, kt * b_ktile, wave);
   }
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
-                                           int wm, int wn, int lane) const {
-    store_rows<T, C>(acc, (T*)g.dxp, g.h, t, wm, wn, lane);
+                                           int wm, int wn, int lane, char* slab) const {
+    store_rows<T, C>(acc, (T*)g.dxp, g.h, t, wm, wn, lane, slab);
   }
 };
 
@@ -1136,7 +1198,7 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
   // tile's extent (elements outside it get an offset past the range).
   static constexpr int kEpiStores = C::MB * C::NB * 4;
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
-                                           int wm, int wn, int lane) const {
+                                           int wm, int wn, int lane, char* slab) const {
     const int Nn = N(g);  // % 64 == 0: a run of 4 columns is all in or all out
     const uint32_t rowb = (uint32_t)Nn * sizeof(float);
     // the tile is the workgroup's: its fields are uniform, which the compiler
@@ -1313,7 +1375,7 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
     }
   }
   next(smem, w, lane);
-  p.epilogue(g, t, acc, wm, wn, lane);
+  p.epilogue(g, t, acc, wm, wn, lane, slab_of<C>(smem, w));
 }
 
 template <typename T, class C, class P>
@@ -1326,7 +1388,7 @@ __device__ __forceinline__ void run_tile(const GemmArgs& g, char* smem, int id, 
 template <typename T, class C, class P>
 __global__ __launch_bounds__(C::kThreads, C::kMinWaves)
 __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_gemm_kernel(GemmArgs g) {
-  __shared__ __attribute__((aligned(1024))) char smem[C::kLds];
+  __shared__ __attribute__((aligned(1024))) char smem[C::kLds + kSlabArea<C>];
   const int n = min((int)gridDim.x, P::total_tiles(g));
   if ((int)blockIdx.x < n) run_tile<T, C, P>(g, smem, blockIdx.x, n);
 }
@@ -1364,12 +1426,15 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
     GemmArgs g) {
   static_assert(C::kThreads == CQ::kThreads && C::kLds >= CQ::kLds, "quarter tiles must fit");
   static_assert(CQ::BM * 2 == C::BM && CQ::BN * 2 == C::BN, "quarter tiles of the same grid");
-  // One LDS object: the stages, then (dynamic launches) the next tile index.
+  // One LDS object: the stages, then the epilogue slabs or (dynamic launches,
+  // whose epilogues take no slab) the next tile index.
   // With a second __shared__ variable the compiler scopes every LDS access
   // by variable and then cannot tell a fragment read of one stage from the
   // copies into the other, so each K step's reads would wait for the next
   // step's copies.
-  __shared__ __attribute__((aligned(1024))) char smem[C::kLds + 16];
+  static_assert(CQ::kLds + kSlabArea<CQ> <= C::kLds + (kSlabArea<C> > 16 ? kSlabArea<C> : 16),
+                "quarter-tile slabs inside the array");
+  __shared__ __attribute__((aligned(1024))) char smem[C::kLds + (kSlabArea<C> > 16 ? kSlabArea<C> : 16)];
   const int tiles = P::total_tiles(g);
   const int full = tiles / g.cus * g.cus, rem = tiles - full;
   const bool split = g.split_tail && 2 * rem <= g.cus;
@@ -1521,7 +1586,7 @@ template <typename T, class C, class PD, class PW>
 __global__ __launch_bounds__(C::kThreads, C::kMinWaves)
 __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_gemm_bwd_pair_kernel(
     GemmArgs g, int nd, int nw) {
-  __shared__ __attribute__((aligned(1024))) char smem[C::kLds];
+  __shared__ __attribute__((aligned(1024))) char smem[C::kLds + kSlabArea<C>];
   const int Kd = PD::reduction(g);
   // first rank (experts by descending rows) with fewer than Kd rows
   int lo = 0, hi = g.E;
