@@ -57,11 +57,30 @@ __global__ __launch_bounds__(256) void combine_kernel(const T* __restrict__ y,
   *(u32x4_t*)(Y + t * h + c * V) = pack16(acc, (T*)nullptr);
 }
 
+// sum of the P per-tile partials of one row, in index order (P = F / 32 is
+// even: 8-byte loads); 0 for a dropped slot (r < 0)
+__device__ __forceinline__ float dgate_of_row(const float* __restrict__ dgp, int P, int r) {
+  float s = 0.f;
+  if (r >= 0) {
+    const f32x2_t* p = (const f32x2_t*)(dgp + (int64_t)r * P);
+    for (int q = 0; q < P / 2; ++q) {
+      const f32x2_t v = p[q];
+      s += v[0];
+      s += v[1];
+    }
+  }
+  return s;
+}
+
+// With dgp set (and k <= h / V), thread c < k of token i also writes the gate
+// gradient of the token's slot c, which saves the separate dgate launch.
 template <typename T>
 __global__ __launch_bounds__(256) void unpermute_kernel(const T* __restrict__ dxp,
                                                         const int32_t* __restrict__ row_of_slot,
                                                         int64_t t0, int tokens, int h, int k,
-                                                        T* __restrict__ dX) {
+                                                        T* __restrict__ dX,
+                                                        const float* __restrict__ dgp, int P,
+                                                        float* __restrict__ dgates) {
   constexpr int V = Elem<T>::kVec;
   const int vpr = h / V;
   const int64_t gid = blockIdx.x * 256ll + threadIdx.x;
@@ -89,6 +108,8 @@ __global__ __launch_bounds__(256) void unpermute_kernel(const T* __restrict__ dx
     }
   }
   *(u32x4_t*)(dX + (t0 + i) * h + c * V) = pack16(acc, (T*)nullptr);
+  if (dgp != nullptr && c < k)
+    dgates[(t0 + i) * k + c] = dgate_of_row(dgp, P, row_of_slot[(int64_t)i * k + c]);
 }
 
 // One thread per slot of the chunk: dgates[slot] = sum over p of dgp[row][p].
@@ -98,17 +119,7 @@ __global__ __launch_bounds__(256) void dgate_kernel(const float* __restrict__ dg
                                                     float* __restrict__ dgates) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= nslots) return;
-  const int r = row_of_slot[i];
-  float s = 0.f;
-  if (r >= 0) {  // P = F / 32 is even: 8-byte loads, summed in index order
-    const f32x2_t* p = (const f32x2_t*)(dgp + (int64_t)r * P);
-    for (int q = 0; q < P / 2; ++q) {
-      const f32x2_t v = p[q];
-      s += v[0];
-      s += v[1];
-    }
-  }
-  dgates[slot0 + i] = s;
+  dgates[slot0 + i] = dgate_of_row(dgp, P, row_of_slot[i]);
 }
 
 hipError_t launch_combine(int dtype, const void* y, const int32_t* row_of_slot, const float* gates,
@@ -133,14 +144,16 @@ hipError_t launch_unpermute(int dtype, const void* dxp, const float* dgp, int P,
   const int64_t work = (int64_t)tokens * (h / V);
   if (work == 0) return hipSuccess;
   const int blocks = (int)((work + 255) / 256);
+  const bool fused = k <= h / V;  // every token has a thread per slot
+  const float* dgp_f = fused ? dgp : nullptr;
   if (dtype == 0)
     unpermute_kernel<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t*)dxp, row_of_slot, t0, tokens, h,
-                                                    k, (bf16_t*)dX);
+                                                    k, (bf16_t*)dX, dgp_f, P, dgates);
   else
     unpermute_kernel<float><<<blocks, 256, 0, s>>>((const float*)dxp, row_of_slot, t0, tokens, h, k,
-                                                   (float*)dX);
+                                                   (float*)dX, dgp_f, P, dgates);
   hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  if (err != hipSuccess || fused) return err;
   const int nslots = tokens * k;
   dgate_kernel<<<(nslots + 255) / 256, 256, 0, s>>>(dgp, P, row_of_slot, t0 * k, nslots, dgates);
   return hipGetLastError();
