@@ -169,6 +169,27 @@ def test_layer_parity_many_experts(mf, E, C):
         assert relerr(host(B[key]), R[key]) <= TOL["bf16"], key
 
 
+@pytest.mark.parametrize("h,k,dtype,C", [(64, 12, "bf16", 2), (128, 12, "bf16", 1),
+                                         (64, 20, "f32", 2), (128, 9, "bf16", 3)])
+def test_layer_parity_large_k(mf, h, k, dtype, C):
+    """More slots per token than 16-byte vectors per row (k > h / 8 in bf16,
+    h / 4 in fp32): the gate-gradient sums run as their own kernel instead of
+    inside the unpermute kernel; and k > 8 takes the combine's slot groups
+    twice."""
+    w = mw.Workload(f"k{k}-h{h}", T=300, h=h, F=128, E=24, k=k, dtype=dtype, routing="dirichlet")
+    case = mw.make_case(w, 7 + k + h)
+    dev = device_case(w, case)
+    log(f"large k: h={h} k={k} {dtype} C={C}")
+    Y = run_fwd(w, dev, C)
+    B = run_bwd(w, dev, C)
+    torch().cuda.synchronize()
+    Y_ref = om.moe_fwd(case["X"], case["idx"], case["gates"], case["W1"], case["W2"], C)
+    R = om.moe_bwd(case["X"], case["idx"], case["gates"], case["W1"], case["W2"], case["dY"], C)
+    assert relerr(host(Y), Y_ref) <= TOL[dtype]
+    for key in ("dX", "dgates", "dW1", "dW2"):
+        assert relerr(host(B[key]), R[key]) <= TOL[dtype], key
+
+
 @pytest.mark.parametrize("name", ["cfg1-f32", "cfg3-like", "cfg4-like"])
 def test_chunk_invariance_and_determinism(mf, name):
     w, case = small_case(name)
