@@ -108,6 +108,9 @@ using Small = Cfg<128, 128, 2, 2, 2>;
 constexpr int kSlabBytes = 32 * 128;
 template <class C> constexpr int kSlabArea =
     C::kLds + C::NW * kSlabBytes <= 160 * 1024 ? C::NW * kSlabBytes : 0;
+// Slab per wave taken from the stages by epilogues that run with no copies
+// in flight.
+constexpr int kStageSlabBytes = 8 * 1024;
 template <class C> __device__ __forceinline__ char* slab_of(char* smem, int wave) {
   if constexpr (kSlabArea<C> > 0) return smem + C::kLds + wave * kSlabBytes;
   else return nullptr;
@@ -176,6 +179,14 @@ __device__ __forceinline__ void store_f32x4(__amdgpu_buffer_rsrc_t r, uint32_t v
 #pragma clang loop unroll(full)
   for (int c = 0; c < 4; ++c) x[c] = v[c];
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, x), r, voff, 0, 0);
+}
+
+// 4 floats as 4 bf16 (8 bytes)
+__device__ __forceinline__ u32x2_t pack4(const float (&f)[4]) {
+  u32x2_t x;
+  x[0] = pack_bf16x2(f[0], f[1]);
+  x[1] = pack_bf16x2(f[2], f[3]);
+  return x;
 }
 
 template <typename T> struct Mma;
@@ -672,6 +683,9 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
   static constexpr int kRaster = 4;  // preferred tile order (XCD blocks, row-major)
   static constexpr bool kEpilogueLoads = kBwd;  // the epilogue reads global memory
   static constexpr int kHalf = C::WTN / 2;
+  // the recomputation's epilogue can stage its stores through LDS (bf16, 32
+  // output columns per wave)
+  static constexpr bool kStaged = kBwd && sizeof(T) == 2 && kHalf == 32;
   typedef KcOp<T, C::BM, C::NW, C::KB, C::DA> OA;
   typedef KcOp<T, C::BN, C::NW, C::KB, C::DB> OB;
   OA A;
@@ -723,7 +737,7 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
                                            int wm, int wn, int lane, char* slab) const {
     if constexpr (kBwd) {
-      epilogue_bwd(g, t, acc, wm, wn, lane);
+      epilogue_bwd(g, t, acc, wm, wn, lane, slab);
     } else {
 #pragma clang loop unroll(full)
       for (int mb = 0; mb < C::MB; ++mb) {
@@ -750,9 +764,13 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
   // Steps walk the row blocks mb; the dA values of block mb + 1 are loaded
   // while block mb is computed and stored (two buffers).  Rows past the tile
   // and column blocks past F load from clamped in-range addresses and are not
-  // used.
+  // used.  With `slab` (bf16, 32 columns per wave: 3 x 2 KB per wave) the
+  // three outputs of a row block go through it: the lanes write their runs
+  // of row lane % 32 (64-byte rows, 16-byte units XOR-swizzled by row), then
+  // read back 16 bytes each, 4 lanes to a row, and store 16 rows x 64 bytes
+  // per instruction.
   __device__ __forceinline__ void epilogue_bwd(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
-                                               int wm, int wn, int lane) const {
+                                               int wm, int wn, int lane, char* slab) const {
     typedef typename Vec4<T>::Raw Raw;
     constexpr int NH = C::NB / 2;  // gate (and up) blocks per wave
     Raw dar[2][NH][4];
@@ -787,6 +805,7 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
         const int fb = t.n0 + wn * kHalf + nb * 32;
         if (fb >= g.F) continue;
         float part = 0.f;
+        const bool staged = kStaged && slab != nullptr;
 #pragma clang loop unroll(full)
         for (int gq = 0; gq < 4; ++gq) {
           float dA[4], gate[4], up[4], dug[4], duu[4], ga[4];
@@ -802,12 +821,37 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
             duu[c] = da * silu;
             ga[c] = gt * act;
           }
-          if (in) {
+          if (staged) {
+            const int rr = lane & 31;
+            const int off = rr * 64 + ((gq ^ (rr & 3)) << 4) + (lane >> 5) * 8;
+            *(u32x2_t*)(slab + off) = pack4(dug);
+            *(u32x2_t*)(slab + 2048 + off) = pack4(duu);
+            *(u32x2_t*)(slab + 4096 + off) = pack4(ga);
+          } else if (in) {
             const int f = fb + gq * 8 + (lane >> 5) * 4;
             Vec4<T>::store(u + f, dug);
             Vec4<T>::store(u + g.F + f, duu);
             Vec4<T>::store(ag + f, ga);
           }
+        }
+        if (staged) {
+          asm volatile("" ::: "memory");  // the writes above before the reads below
+          const int unit = lane & 3;
+#pragma clang loop unroll(full)
+          for (int o = 0; o < 3; ++o)
+#pragma clang loop unroll(full)
+            for (int q = 0; q < 2; ++q) {
+              const int r2 = (lane >> 2) + 16 * q;
+              const u32x4_t x = *(const u32x4_t*)(slab + o * 2048 + r2 * 64 + ((unit ^ (r2 & 3)) << 4));
+              const int rt = wm * C::WTM + mb * 32 + r2;
+              if (rt < t.mrows) {
+                const int64_t row2 = t.m0 + rt;
+                const int f = fb + unit * 8;
+                T* dst = o == 2 ? (T*)g.ag + row2 * g.F + f : (T*)g.u + row2 * 2 * g.F + o * g.F + f;
+                *(u32x4_t*)dst = x;
+              }
+            }
+          asm volatile("" ::: "memory");  // the reads above before the next writes
         }
         // the row's 32 columns of the block are split between lanes l and l + 32
         part += __shfl_xor(part, 32, 64);
@@ -1375,7 +1419,15 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
     }
   }
   next(smem, w, lane);
-  p.epilogue(g, t, acc, wm, wn, lane, slab_of<C>(smem, w));
+  char* slab = slab_of<C>(smem, w);
+  if constexpr (P::kEpilogueLoads && C::NW * kStageSlabBytes <= C::kLds) {
+    // No copies of a next tile are in flight during such an epilogue (they
+    // are issued after it): once every wave is past its last multiply, the
+    // stages are free and each wave takes kStageSlabBytes of them.
+    __syncthreads();
+    slab = smem + w * kStageSlabBytes;
+  }
+  p.epilogue(g, t, acc, wm, wn, lane, slab);
 }
 
 template <typename T, class C, class P>
