@@ -104,10 +104,11 @@ using Small = Cfg<128, 128, 2, 2, 2>;
 // pieces.  Bounced through a wave-private LDS slab of 32 rows x 128 bytes
 // (16-byte units XOR-swizzled by row), each instruction writes 8 rows x 128
 // contiguous bytes instead.  The slabs sit after the stages (wave w at
-// kLds + w * kSlabBytes), where the LDS has room.
+// kLds + w * kSlabBytes), where the LDS has room without costing a
+// workgroup per CU.
 constexpr int kSlabBytes = 32 * 128;
 template <class C> constexpr int kSlabArea =
-    C::kLds + C::NW * kSlabBytes <= 160 * 1024 ? C::NW * kSlabBytes : 0;
+    (C::kLds + C::NW * kSlabBytes) * C::kWgPerCu <= 160 * 1024 ? C::NW * kSlabBytes : 0;
 // Slab per wave taken from the stages by epilogues that run with no copies
 // in flight.
 constexpr int kStageSlabBytes = 8 * 1024;
