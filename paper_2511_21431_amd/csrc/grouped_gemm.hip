@@ -112,8 +112,11 @@ template <class C> constexpr int kSlabArea =
 // Slab per wave taken from the stages by epilogues that run with no copies
 // in flight.
 constexpr int kStageSlabBytes = 8 * 1024;
-template <class C> __device__ __forceinline__ char* slab_of(char* smem, int wave) {
-  if constexpr (kSlabArea<C> > 0) return smem + C::kLds + wave * kSlabBytes;
+// kArray: bytes of the LDS array the tile runs in (0: a launch of C's own,
+// sized C::kLds + kSlabArea<C>)
+template <class C, int kArray = 0> __device__ __forceinline__ char* slab_of(char* smem, int wave) {
+  constexpr bool fits = kArray > 0 ? C::kLds + C::NW * kSlabBytes <= kArray : kSlabArea<C> > 0;
+  if constexpr (fits) return smem + C::kLds + wave * kSlabBytes;
   else return nullptr;
 }
 
@@ -1348,7 +1351,7 @@ constexpr int vm_cap(int n) { return n < 62 ? n : 62; }
 // stores, were issued after the copies waited for.  Vector-memory
 // instructions retire in order, so waiting until only that many are in
 // flight suffices, and the stores drain under the first two K steps.
-template <typename T, class C, class P, class Next = NoNext>
+template <typename T, class C, class P, int kArray = 0, class Next = NoNext>
 __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p, const Tile& t,
                                             bool prefetched = false, Next next = Next(),
                                             bool deep = false) {
@@ -1420,7 +1423,7 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
     }
   }
   next(smem, w, lane);
-  char* slab = slab_of<C>(smem, w);
+  char* slab = slab_of<C, kArray>(smem, w);
   if constexpr (P::kEpilogueLoads && C::NW * kStageSlabBytes <= C::kLds) {
     // No copies of a next tile are in flight during such an epilogue (they
     // are issued after it): once every wave is past its last multiply, the
@@ -1485,9 +1488,8 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
   // by variable and then cannot tell a fragment read of one stage from the
   // copies into the other, so each K step's reads would wait for the next
   // step's copies.
-  static_assert(CQ::kLds + kSlabArea<CQ> <= C::kLds + (kSlabArea<C> > 16 ? kSlabArea<C> : 16),
-                "quarter-tile slabs inside the array");
-  __shared__ __attribute__((aligned(1024))) char smem[C::kLds + (kSlabArea<C> > 16 ? kSlabArea<C> : 16)];
+  constexpr int kArray = C::kLds + (kSlabArea<C> > 16 ? kSlabArea<C> : 16);
+  __shared__ __attribute__((aligned(1024))) char smem[kArray];
   const int tiles = P::total_tiles(g);
   const int full = tiles / g.cus * g.cus, rem = tiles - full;
   const bool split = g.split_tail && 2 * rem <= g.cus;
@@ -1537,7 +1539,7 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
         PQ pq;
         Tile tq;
         __syncthreads();  // the previous tile's waves are done with the stages
-        if (pq.locate_sub(g, tq, full + q / 4, q % 4)) run_located<T, CQ, PQ>(g, smem, pq, tq);
+        if (pq.locate_sub(g, tq, full + q / 4, q % 4)) run_located<T, CQ, PQ, kArray>(g, smem, pq, tq);
       }
     }
   } else if (kDynamic<C, P> && g.tile_ctr != nullptr) {
@@ -1605,7 +1607,7 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
         PQ pq;
         Tile tq;
         __syncthreads();  // the previous tile's waves are done with the stages
-        if (pq.locate_sub(g, tq, full + q / 4, q % 4)) run_located<T, CQ, PQ>(g, smem, pq, tq);
+        if (pq.locate_sub(g, tq, full + q / 4, q % 4)) run_located<T, CQ, PQ, kArray>(g, smem, pq, tq);
       }
     }
   } else {
@@ -1619,7 +1621,7 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
       PQ p;
       Tile t;
       const int q = id - full;
-      if (p.locate_sub(g, t, full + q / 4, q % 4)) run_located<T, CQ, PQ>(g, smem, p, t);
+      if (p.locate_sub(g, t, full + q / 4, q % 4)) run_located<T, CQ, PQ, kArray>(g, smem, p, t);
     }
   }
 }
