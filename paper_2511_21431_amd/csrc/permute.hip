@@ -5,8 +5,9 @@
 //
 // The grouping is deterministic and stable without atomics on output
 // cursors: each workgroup owns a fixed, ordered range of slots; a first pass
-// counts experts per workgroup, a single-workgroup scan turns the
-// (expert, workgroup) counts into first output rows, and a second pass ranks
+// counts experts per workgroup, a scan turns the (expert, workgroup) counts
+// into first output rows (a single-workgroup kernel, or, while there are few
+// counts, each workgroup of the second pass for itself), and a second pass ranks
 // the slots of each workgroup in order with wavefront ballots (the set of
 // lanes holding the same expert id is found bit by bit) and per-wave counts
 // in LDS.
@@ -106,6 +107,33 @@ __global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ 
   }
 }
 
+// Exclusive scan over v[0..m) in place (one workgroup of 256 threads, m any
+// size): each thread scans a contiguous run, the run totals are scanned in
+// LDS, then each run is offset.  `part` is 256 ints of LDS.  Returns the total.
+__device__ int32_t block_exclusive_scan(int32_t* v, int m, int32_t* part) {
+  const int tid = threadIdx.x, per = (m + 255) / 256;
+  const int a = min(m, tid * per), b = min(m, a + per);
+  int32_t sum = 0;
+  for (int i = a; i < b; ++i) sum += v[i];
+  part[tid] = sum;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int32_t x = tid >= off ? part[tid - off] : 0;
+    __syncthreads();
+    part[tid] += x;
+    __syncthreads();
+  }
+  int32_t run = part[tid] - sum;
+  const int32_t total = part[255];
+  for (int i = a; i < b; ++i) {
+    const int32_t x = v[i];
+    v[i] = run;
+    run += x;
+  }
+  __syncthreads();
+  return total;
+}
+
 // Stable scatter (an id outside [0, E) - which memfine_count reports - is
 // dropped: it gets no row and row_of_slot = -1).  Workgroup b walks its slot
 // range in rounds of 256 slots (4 waves x 64 lanes, in slot order; with 256
@@ -114,16 +142,61 @@ __global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ 
 //   first row of (expert, b) + slots of that expert in earlier rounds
 //   + slots of that expert in earlier waves of this round + its rank among
 //   the lanes of its own wave holding the same expert.
+//
+// kFused: the workgroup derives its first rows from the per-block counts
+// itself (the total of every expert over all blocks, scanned over experts,
+// plus the expert's slots in earlier blocks), and workgroup 0 writes counts,
+// offsets and order, which saves the single-workgroup scan launch; used
+// while E * nb is small enough that every workgroup reading all counts is
+// cheap.
+template <bool kFused>
 __global__ __launch_bounds__(256) void scatter_kernel(
     const int32_t* __restrict__ idx, const float* __restrict__ gates, int n, int E, int k,
     int slot0, int nb, int spb, const int32_t* __restrict__ bstart, int32_t* __restrict__ sorted_slot,
     int32_t* __restrict__ row_of_slot, int32_t* __restrict__ tok_of_row,
-    float* __restrict__ gate_of_row) {
+    float* __restrict__ gate_of_row, const int32_t* __restrict__ bcount,
+    int32_t* __restrict__ counts, int32_t* __restrict__ offsets, int32_t* __restrict__ order) {
   extern __shared__ int32_t sh[];
   int32_t* run = sh;      // [E]     next row per expert for this workgroup
   int32_t* wc = sh + E;   // [4][E]  per-wave counts of the current round
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  for (int e = tid; e < E; e += 256) run[e] = bstart[(int64_t)e * nb + blockIdx.x];
+  if constexpr (kFused) {
+    int32_t* tot = wc;           // [E] slots of each expert in the chunk, then its first row
+    int32_t* pre = wc + E;       // [E] the expert's slots in the workgroups before this one
+    int32_t* cnt = wc + 2 * E;   // [E] the counts, kept for the order
+    __shared__ int32_t spart[256];
+    for (int e = tid; e < E; e += 256) tot[e] = pre[e] = 0;
+    __syncthreads();
+    const int64_t m = (int64_t)E * nb;
+    for (int64_t i = tid; i < m; i += 256) {
+      const int32_t v = bcount[i];
+      if (v) {
+        const int e = (int)(i / nb), b = (int)(i % nb);
+        atomicAdd(&tot[e], v);
+        if (b < (int)blockIdx.x) atomicAdd(&pre[e], v);
+      }
+    }
+    __syncthreads();
+    for (int e = tid; e < E; e += 256) cnt[e] = tot[e];
+    __syncthreads();
+    const int32_t total = block_exclusive_scan(tot, E, spart);
+    for (int e = tid; e < E; e += 256) run[e] = tot[e] + pre[e];
+    if (blockIdx.x == 0) {
+      for (int e = tid; e < E; e += 256) {
+        counts[e] = cnt[e];
+        offsets[e] = tot[e];
+        // order: experts by descending count, ties by id
+        const int32_t c = cnt[e];
+        int rank = 0;
+        for (int e2 = 0; e2 < E; ++e2) rank += (cnt[e2] > c) || (cnt[e2] == c && e2 < e);
+        order[rank] = e;
+      }
+      if (tid == 0) offsets[E] = total;
+    }
+    __syncthreads();
+  } else {
+    for (int e = tid; e < E; e += 256) run[e] = bstart[(int64_t)e * nb + blockIdx.x];
+  }
   for (int i = tid; i < 4 * E; i += 256) wc[i] = 0;
   __syncthreads();
   const int nbits = E > 1 ? 32 - __clz(E - 1) : 0;
@@ -187,13 +260,22 @@ hipError_t launch_dispatch(const int32_t* idx, const float* gates, int64_t slot0
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
   }
-  scan_kernel<<<1, 1024, 0, s>>>(m.bcount, E, nb, n, m.bstart, m.counts, m.offsets, m.order);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess || nb == 0) return err;
-  scatter_kernel<<<nb, 256, 5 * E * sizeof(int32_t), s>>>(
-      cidx, gates ? gates + slot0 : nullptr, n, E, k, (int)slot0, nb, spb, m.bstart, m.sorted_slot,
-      m.row_of_slot,
-      m.tok_of_row, m.gate_of_row);
+  // small E x nb: the scatter workgroups scan the counts themselves
+  const bool fused = nb > 0 && (int64_t)E * nb <= 16384;
+  if (!fused) {
+    scan_kernel<<<1, 1024, 0, s>>>(m.bcount, E, nb, n, m.bstart, m.counts, m.offsets, m.order);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess || nb == 0) return err;
+    scatter_kernel<false><<<nb, 256, 5 * E * sizeof(int32_t), s>>>(
+        cidx, gates ? gates + slot0 : nullptr, n, E, k, (int)slot0, nb, spb, m.bstart,
+        m.sorted_slot, m.row_of_slot, m.tok_of_row, m.gate_of_row, nullptr, nullptr, nullptr,
+        nullptr);
+  } else {
+    scatter_kernel<true><<<nb, 256, 5 * E * sizeof(int32_t), s>>>(
+        cidx, gates ? gates + slot0 : nullptr, n, E, k, (int)slot0, nb, spb, m.bstart,
+        m.sorted_slot, m.row_of_slot, m.tok_of_row, m.gate_of_row, m.bcount, m.counts, m.offsets,
+        m.order);
+  }
   return hipGetLastError();
 }
 
