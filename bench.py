@@ -35,6 +35,9 @@ PEAK_HBM_GBS = 8000.0
 # activation budget handed to the planner per workload (bytes); the plan
 # then picks C from the bins
 DEFAULT_BUDGET = {1: 64 * 1024, 2: 250 * 10**6, 3: 500 * 10**6, 4: 10**9, 5: 8 * 10**9}
+# activation budgets swept through the planner (workload 5: 4 GB to 64 GB);
+# each budget's C is joined with the measured chunk sweep
+BUDGET_SWEEP = {5: [4 * 10**9, 8 * 10**9, 16 * 10**9, 32 * 10**9, 64 * 10**9]}
 
 
 def log(msg):
@@ -222,6 +225,27 @@ def main():
             })
             log(f"[bench] sweep C={Cs}: {tps:.0f} tokens/s, peak activation {peak_b / 1e9:.3f} GB")
 
+    # ---- activation-budget sweep: the planner's C per budget (Eq. (8)/(9) +
+    # bins from this workload's counts), with that C's measured throughput
+    # and peak activation from the chunk sweep
+    budget_sweep = None
+    if cfg in BUDGET_SWEEP:
+        counts = mf.memfine_count(shape, idx, work)
+        by_c = {r["chunks"]: r for r in sweep}
+        budget_sweep = []
+        for b in BUDGET_SWEEP[cfg]:
+            rc_b, C_b, info_b = mf.memfine_plan(shape, counts, b, bins=bins)
+            r = by_c.get(C_b, {})
+            budget_sweep.append({
+                "budget_bytes": b, "status": mf.memfine_status_str(rc_b), "chunks": C_b,
+                "c_theory": info_b["c_theory"],
+                "tokens_per_s": r.get("tokens_per_s"),
+                "peak_activation_bytes": r.get("peak_activation_bytes"),
+                "predicted_bytes_paper_model": r.get("predicted_bytes_paper_model"),
+                "within_budget": (r["peak_activation_bytes"] <= b) if r else None})
+            log(f"[bench] budget {b / 1e9:.0f} GB: C={C_b} (c={info_b['c_theory']}), "
+                f"{r.get('tokens_per_s')} tokens/s, peak {r.get('peak_activation_bytes')} B")
+
     # ---- the router in front of the layer: its kernels, and the whole block
     router = None
     if not args.no_router and w.E <= 64 and w.k <= 16:
@@ -270,6 +294,7 @@ def main():
                              for k, v in prof_all.items()},
         "layer_roofline_frac": round(layer_bound_ms(prof_all, peak) / ms_per_step, 4),
         "chunks_sweep": sweep,
+        "budget_sweep": budget_sweep,
         "router": router,
         "cpu_baseline": cpu,
     }
