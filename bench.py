@@ -60,6 +60,13 @@ def parse():
                     help="target duration of the oracle sample")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one plain 1 GiB device copy first (reference for HBM counters)")
+    ap.add_argument("--summarize-traffic", metavar="DIR", default=None,
+                    help="no GPU work: turn the FETCH_SIZE / WRITE_SIZE counter CSVs of two "
+                         "rocprofv3 --pmc runs in DIR into profiles/fc1_wgrad_cfg<N>_traffic.json")
+    ap.add_argument("--summarize-mfma", metavar="CSV", default=None,
+                    help="no GPU work: print a per-kernel MFMA utilisation table from a "
+                         "rocprofv3 --pmc CSV of SQ_VALU_MFMA_BUSY_CYCLES, "
+                         "SQ_INSTS_VALU_MFMA_MOPS_BF16, GRBM_GUI_ACTIVE")
     return ap.parse_args()
 
 
@@ -86,8 +93,109 @@ def read_traffic(kernel: str, workload: str):
         return None
 
 
+# ---- counter summaries (host only) ----------------------------------------
+# The FC1 weight-gradient launches of the split-tail grid (whole tiles of the
+# 256 x 256, 8-wave configuration); the two dW modes are separate kernels.
+FC1_WGRAD_KEY = ("grouped_gemm_split_kernel",
+                 "ProbWgrad<unsigned short, memfine::(anonymous namespace)::Cfg<256, 256, 2, 4, 2, 128, 3>, true, ")
+
+
+def _counter_rows(path):
+    import csv
+    with open(path, newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def summarize_traffic(d, cfg):
+    """HBM bytes per FC1 weight-gradient launch from two counter runs, each
+    counter scaled by what it reads for the 1 GiB elementwise pass
+    (`--calibrate-copy`, kernel neg) in the same process."""
+    per = {}
+    scale = {}
+    for ctr, key in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write")):
+        rows = _counter_rows(os.path.join(d, f"{ctr}_counter_collection.csv"))
+        ref = [float(r["Counter_Value"]) for r in rows if "neg_kernel" in r["Kernel_Name"]]
+        if len(ref) != 1:
+            raise SystemExit(f"{ctr}: expected one calibration dispatch, found {len(ref)}")
+        scale[key] = (1 << 30) / (ref[0] * 1024.0)      # counter in KiB
+        scale[key + "_kb"] = ref[0]
+        for r in rows:
+            n = r["Kernel_Name"]
+            if all(k in n for k in FC1_WGRAD_KEY):
+                e = per.setdefault(n, {"launches": 0, "fetch_bytes": 0.0, "write_bytes": 0.0})
+                if key == "fetch":
+                    e["launches"] += 1
+                e[key + "_bytes"] += float(r["Counter_Value"]) * 1024.0 * scale[key]
+    if not per:
+        raise SystemExit("no FC1 weight-gradient dispatches in the counter files")
+    for e in per.values():
+        e["fetch_bytes"] /= e["launches"]
+        e["write_bytes"] /= e["launches"]
+    # mean over the two dW modes, one launch of each per step
+    fetch = sum(e["fetch_bytes"] for e in per.values()) / len(per)
+    write = sum(e["write_bytes"] for e in per.values()) / len(per)
+    out = {"kernel": "fc1_wgrad", "rocprof_name": " + ".join(sorted(per)),
+           "launches_profiled": sum(e["launches"] for e in per.values()), "per_kernel": per,
+           "fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,
+           "bytes_per_launch": fetch + write,
+           "copy_reference": {"bytes_each_way": float(1 << 30), "fetch_kb": scale["fetch_kb"],
+                              "write_kb": scale["write_kb"], "fetch_scale": scale["fetch"],
+                              "write_scale": scale["write"]},
+           "source": "grouped_gemm.hip", "source_sha256_16": source_digest("grouped_gemm.hip")}
+    path = os.path.join(ROOT, "profiles", f"fc1_wgrad_cfg{cfg}_traffic.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(f"{path}: fetch {fetch:.4g} B + write {write:.4g} B per launch")
+    for n, e in sorted(per.items()):
+        print(f"  {n[-12:]}: {e['launches']} launches, fetch {e['fetch_bytes']:.4g}, "
+              f"write {e['write_bytes']:.4g}")
+
+
+def summarize_mfma(path):
+    """Per GEMM kernel: MFMA busy share (rocprofv3's MfmaUtil: busy cycles
+    summed over the SIMDs / (GUI-active cycles of one XCD x 1024 SIMDs); the
+    CSV's GRBM_GUI_ACTIVE is the sum over the 8 XCDs) and the bf16 MFMA
+    flops the matrix cores executed (MOPS x 512) against the dispatch time."""
+    import re
+    rows = _counter_rows(path)
+    disp = {}
+    for r in rows:
+        e = disp.setdefault(r["Dispatch_Id"], {"name": r["Kernel_Name"], "ns":
+                            int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
+        e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    agg = {}
+    for e in disp.values():
+        m = re.search(r"(Prob\w+)<unsigned short, [^<]*Cfg<256, 256[^>]*>(?:, (true|false))?(?:, (\d))?",
+                      e["name"])
+        if not m or "split" not in e["name"]:
+            continue
+        k = {"ProbFC1": "fc1_recompute" if m.group(2) == "true" else "fc1", "ProbFC2": "fc2",
+             "ProbFC2Dgrad": "fc2_dgrad", "ProbFC1Dgrad": "fc1_dgrad",
+             "ProbWgrad": ("fc1_wgrad" if m.group(2) == "true" else "fc2_wgrad")
+             + (", dW accumulated" if m.group(3) == "1" else ", dW written")}[m.group(1)]
+        a = agg.setdefault(k, {"n": 0, "ns": 0, "busy": 0.0, "gui": 0.0, "mops": 0.0})
+        a["n"] += 1
+        a["ns"] += e["ns"]
+        a["busy"] += e.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+        a["gui"] += e.get("GRBM_GUI_ACTIVE", 0.0)
+        a["mops"] += e.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)
+    print("| kernel | launches | avg us | MFMA busy (MfmaUtil) | executed bf16 TFLOP/s | of 2.5 PFLOP/s |")
+    print("|---|---:|---:|---:|---:|---:|")
+    for k, a in sorted(agg.items(), key=lambda kv: -kv[1]["ns"]):
+        util = a["busy"] / (a["gui"] / 8.0 * 1024.0)
+        tf = a["mops"] * 512.0 / (a["ns"] * 1e-9) / 1e12
+        print(f"| {k} | {a['n']} | {a['ns'] / a['n'] / 1e3:.1f} | {util * 100:.1f} % | {tf:.0f} | "
+              f"{tf / PEAK_TFLOPS['bf16'] * 100:.1f} % |")
+
+
 def main():
     args = parse()
+    if args.summarize_traffic:
+        summarize_traffic(args.summarize_traffic, args.config)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(args.summarize_mfma)
+        return
     if args.gpus != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
               "(the expert-parallel exchange is out of scope), so --gpus must be 1",
