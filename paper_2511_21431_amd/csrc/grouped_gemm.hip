@@ -68,6 +68,14 @@ constexpr bool kSchedHints = MEMFINE_SCHED_HINTS;
 #define MEMFINE_MMA_PRIO 2
 #endif
 constexpr int kMmaPrio = MEMFINE_MMA_PRIO;
+// The direct-copy loops instead raise it from the K step's wait through the
+// barrier and the issue of the next K tile's copies, so that the copies go
+// out before the other wave's MFMAs take the issue slots (-0.3-0.4 % step
+// time; priority during their MFMAs measured 1-2 % slower).
+#ifndef MEMFINE_DIRECT_PRIO
+#define MEMFINE_DIRECT_PRIO 1
+#endif
+constexpr int kDirectPrio = MEMFINE_DIRECT_PRIO;
 
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
@@ -1387,6 +1395,7 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
   if constexpr (C::DIRECT) {
     if (!prefetched) issue_prologue<T, C, P>(g, smem, p, t, w, lane);
     for (int kt = 0; kt < nk; ++kt) {
+      if constexpr (kDirectPrio == 1) __builtin_amdgcn_s_setprio(2);
       if constexpr (kDeep<C, P>) {
         if (deep && kt == 0 && nk > 1) wait_vm<vm_cap(kCopies + P::kEpiStores)>();
         else if (deep && kt < 2) wait_vm<vm_cap(P::kEpiStores)>();
@@ -1406,6 +1415,7 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
         char* st = smem + ((kt + C::S - 1) % C::S) * C::kStage;
         p.issue(g, t, kt + C::S - 1, st, st + C::BM * C::KB, w, lane);
       }
+      if constexpr (kDirectPrio == 1) __builtin_amdgcn_s_setprio(0);
       char* cur = smem + (kt % C::S) * C::kStage;
       if (active)
         mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
