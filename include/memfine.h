@@ -13,11 +13,13 @@
  * ---------------------------------------
  * - Pointers named d_* are device pointers, h_* host pointers.  Every buffer
  *   is owned by the caller; the library keeps no state between calls except a
- *   lazily created per-process profiling table, for calls made with a NULL
- *   allocator one lazily created stream-ordered memory pool per device (its
- *   freed chunk memory is kept for reuse until the process ends), and, only
- *   when MEMFINE_STREAMS=1 is set, two side streams and three events per
- *   device (kept until the process ends).
+ *   lazily created per-process profiling table; for calls made with a NULL
+ *   allocator, one workspace block per (device, stream), carved into each
+ *   chunk's buffers and reused by the next chunk in stream order (grown from
+ *   a per-device stream-ordered pool when a call needs more, never shrunk,
+ *   kept until the process ends); one pinned host buffer of 1025 ints per
+ *   device for memfine_count; and, only when MEMFINE_STREAMS=1 is set, two
+ *   side streams and three events per device (kept until the process ends).
  * - Environment variables MEMFINE_TILE, MEMFINE_RASTER, MEMFINE_SPLIT,
  *   MEMFINE_PAIR and MEMFINE_STREAMS, read at every call, select alternative
  *   GEMM tile shapes, tile orders and launch schedules for measurement; every
@@ -87,8 +89,10 @@ typedef struct memfine_shape {
  * alloc(bytes, stream, ctx) returns a device pointer (256-byte aligned) that
  * is usable in stream order on `stream`, or NULL on failure; release(ptr,
  * bytes, stream, ctx) gives it back in stream order.  When the allocator
- * argument of a call is NULL the library uses hipMallocAsync/hipFreeAsync on
- * the call's stream.
+ * argument of a call is NULL the library takes the chunk's buffers from its
+ * cached workspace block for the call's stream (see the conventions above):
+ * the block's size is the largest per-chunk workspace asked for on that
+ * stream so far, and it stays allocated after the call returns.
  */
 typedef struct memfine_allocator {
   void* (*alloc)(size_t bytes, void* stream, void* ctx);

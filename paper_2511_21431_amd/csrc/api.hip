@@ -4,6 +4,7 @@
 // (paper Section 4.1, Eq. (6)/(7); Section 4.2, Eq. (8)/(9)).
 #include <algorithm>
 #include <cstdlib>
+#include <map>
 #include <mutex>
 #include <unordered_map>
 #include <vector>
@@ -148,9 +149,25 @@ hipMemPool_t device_pool() {
   return pool;
 }
 
-void* ws_alloc(const memfine_allocator* a, size_t bytes, hipStream_t s) {
-  if (bytes == 0) bytes = 256;
-  if (a && a->alloc) return a->alloc(bytes, (void*)s, a->ctx);
+// Calls with a NULL allocator carve each chunk's buffers from one cached
+// block per (device, stream) and hand it back when the chunk ends.  Kernels
+// on one stream run in order, so the next chunk (or call) on that stream may
+// take the block again at once, with no trip to the allocator: a
+// hipFreeAsync per chunk blocked the host for up to ~1 ms here, long enough
+// that the next chunk's kernels were enqueued only after the GPU had
+// drained.  The block is re-allocated (from the pool, in stream order) when
+// a larger workspace is asked for and kept until the process ends.  A
+// request while the stream's block is taken gets a pool allocation of its
+// own.
+struct WsBlock {
+  void* p = nullptr;
+  size_t bytes = 0;
+  bool busy = false;
+};
+std::mutex g_ws_mu;
+std::map<std::pair<int, hipStream_t>, WsBlock> g_ws;
+
+void* pool_alloc(size_t bytes, hipStream_t s) {
   hipMemPool_t pool = device_pool();
   if (!pool) return nullptr;
   void* p = nullptr;
@@ -161,12 +178,53 @@ void* ws_alloc(const memfine_allocator* a, size_t bytes, hipStream_t s) {
   return p;
 }
 
+void* ws_alloc(const memfine_allocator* a, size_t bytes, hipStream_t s) {
+  if (bytes == 0) bytes = 256;
+  if (a && a->alloc) return a->alloc(bytes, (void*)s, a->ctx);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    WsBlock& b = g_ws[{dev, s}];
+    if (!b.busy) {
+      if (b.bytes < bytes) {
+        if (b.p) (void)hipFreeAsync(b.p, s);
+        b.p = pool_alloc(bytes, s);
+        b.bytes = b.p ? bytes : 0;
+        if (!b.p) return nullptr;
+      }
+      b.busy = true;
+      return b.p;
+    }
+  }
+  return pool_alloc(bytes, s);
+}
+
 void ws_release(const memfine_allocator* a, void* p, size_t bytes, hipStream_t s) {
   if (!p) return;
   if (bytes == 0) bytes = 256;
-  if (a && a->release) a->release(p, bytes, (void*)s, a->ctx);
-  else if (!(a && a->alloc)) (void)hipFreeAsync(p, s);
+  if (a && a->release) {
+    a->release(p, bytes, (void*)s, a->ctx);
+    return;
+  }
+  if (a && a->alloc) return;
+  int dev = 0;
+  if (hipGetDevice(&dev) == hipSuccess) {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    auto it = g_ws.find({dev, s});
+    if (it != g_ws.end() && it->second.p == p) {
+      it->second.busy = false;
+      return;
+    }
+  }
+  (void)hipFreeAsync(p, s);
 }
+
+// Pinned host buffer per device for memfine_count's result (E + 1 ints at
+// most 1025), allocated on first use and kept until the process ends.
+constexpr int kMaxExperts = 1024;
+std::mutex g_pinned_mu;
+std::unordered_map<int, int32_t*> g_pinned;
 
 struct ChunkBuffers {
   ChunkMeta m;
@@ -407,13 +465,23 @@ int memfine_count(const memfine_shape* shape, const int32_t* d_idx, int32_t* d_w
   if (!d_work || !h_counts || (shape->T > 0 && !d_idx)) return MEMFINE_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
   const int64_t nslots = shape->T * shape->k;
-  std::vector<int32_t> host(shape->E + 1, 0);
   {
     KernelTimer kt(MEMFINE_K_COUNT, s, 0.0, 4.0 * nslots);
     if (launch_count(d_idx, nslots, shape->E, d_work, s) != hipSuccess) return MEMFINE_ERR_HIP;
   }
-  if (hipMemcpyAsync(host.data(), d_work, (shape->E + 1) * sizeof(int32_t), hipMemcpyDeviceToHost,
-                     s) != hipSuccess)
+  // the counts come back through a pinned buffer (a direct copy; a pageable
+  // destination is staged by the runtime)
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MEMFINE_ERR_HIP;
+  std::lock_guard<std::mutex> lk(g_pinned_mu);
+  int32_t*& host = g_pinned[dev];
+  if (!host && hipHostMalloc((void**)&host, (kMaxExperts + 1) * sizeof(int32_t),
+                             hipHostMallocDefault) != hipSuccess) {
+    host = nullptr;
+    return MEMFINE_ERR_HIP;
+  }
+  if (hipMemcpyAsync(host, d_work, (shape->E + 1) * sizeof(int32_t), hipMemcpyDeviceToHost, s) !=
+      hipSuccess)
     return MEMFINE_ERR_HIP;
   if (hipStreamSynchronize(s) != hipSuccess) return MEMFINE_ERR_HIP;
   for (int e = 0; e < shape->E; ++e) h_counts[e] = host[e];
