@@ -225,6 +225,36 @@ def test_side_stream_backward_bitwise(mf, monkeypatch):
             assert np.array_equal(got[key], ref[key]), (C, key)
 
 
+def test_internal_workspace_per_stream(mf):
+    """Calls without an allocator take their chunk buffers from a cached
+    block per (device, stream).  Work enqueued on two streams at once, and a
+    call with larger chunks after one with smaller chunks on the same stream
+    (the stream's block grows), give bit-identical results to the same calls
+    run one by one on the default stream."""
+    t = torch()
+    wa, ca = small_case("cfg2-like")
+    wb, cb = small_case("cfg4-like")
+    da, db = device_case(wa, ca), device_case(wb, cb)
+    ref = {}
+    for name, w, d in (("a", wa, da), ("b", wb, db)):
+        ref[name] = {"Y": host(run_fwd(w, d, 3)), **{k: host(v) for k, v in run_bwd(w, d, 3).items()}}
+    t.cuda.synchronize()
+    s1, s2 = t.cuda.Stream(), t.cuda.Stream()
+    got = {}
+    with t.cuda.stream(s1):
+        run_fwd(wa, da, 7)                   # smaller chunks first: the block grows below
+    for rep in range(2):
+        log(f"two streams, repetition {rep}")
+        with t.cuda.stream(s1):
+            got["a"] = {"Y": run_fwd(wa, da, 3), **run_bwd(wa, da, 3)}
+        with t.cuda.stream(s2):
+            got["b"] = {"Y": run_fwd(wb, db, 3), **run_bwd(wb, db, 3)}
+        t.cuda.synchronize()
+        for name in ("a", "b"):
+            for key, v in got[name].items():
+                assert np.array_equal(host(v), ref[name][key]), (rep, name, key)
+
+
 def test_accumulate_dW(mf):
     w, case = small_case("cfg2-like")
     t = torch()
