@@ -137,7 +137,7 @@ int memfine_count(const memfine_shape* shape, const int32_t* d_idx, int32_t* d_w
  *                                  slot id inside an expert (stable)
  *   d_row_of_slot  int32 [n]       row of slot t0*k + i in that order
  * Precondition: ids already validated (memfine_count).  Scratch comes from
- * `alloc` (NULL = hipMallocAsync).  Asynchronous.
+ * `alloc` (NULL = the library's workspace block for the stream).  Asynchronous.
  */
 int memfine_dispatch(const memfine_shape* shape, const int32_t* d_idx, int64_t t0, int64_t t1,
                      int32_t* d_counts, int32_t* d_offsets, int32_t* d_sorted_slot,
