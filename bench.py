@@ -106,10 +106,12 @@ def _counter_rows(path):
         return list(csv.DictReader(f))
 
 
-def summarize_traffic(d, cfg):
+def summarize_traffic(d, cfg, path=None):
     """HBM bytes per FC1 weight-gradient launch from two counter runs, each
     counter scaled by what it reads for the 1 GiB elementwise pass
-    (`--calibrate-copy`, kernel neg) in the same process."""
+    (`--calibrate-copy`, kernel neg) in the same process.  Writes the summary
+    to `path` (default profiles/fc1_wgrad_cfg<cfg>_traffic.json) and returns
+    it."""
     per = {}
     scale = {}
     for ctr, key in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write")):
@@ -142,13 +144,15 @@ def summarize_traffic(d, cfg):
                               "write_kb": scale["write_kb"], "fetch_scale": scale["fetch"],
                               "write_scale": scale["write"]},
            "source": "grouped_gemm.hip", "source_sha256_16": source_digest("grouped_gemm.hip")}
-    path = os.path.join(ROOT, "profiles", f"fc1_wgrad_cfg{cfg}_traffic.json")
+    if path is None:
+        path = os.path.join(ROOT, "profiles", f"fc1_wgrad_cfg{cfg}_traffic.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
     print(f"{path}: fetch {fetch:.4g} B + write {write:.4g} B per launch")
     for n, e in sorted(per.items()):
         print(f"  {n[-12:]}: {e['launches']} launches, fetch {e['fetch_bytes']:.4g}, "
               f"write {e['write_bytes']:.4g}")
+    return out
 
 
 def summarize_mfma(path):
@@ -182,10 +186,11 @@ def summarize_mfma(path):
     print("| kernel | launches | avg us | MFMA busy (MfmaUtil) | executed bf16 TFLOP/s | of 2.5 PFLOP/s |")
     print("|---|---:|---:|---:|---:|---:|")
     for k, a in sorted(agg.items(), key=lambda kv: -kv[1]["ns"]):
-        util = a["busy"] / (a["gui"] / 8.0 * 1024.0)
-        tf = a["mops"] * 512.0 / (a["ns"] * 1e-9) / 1e12
-        print(f"| {k} | {a['n']} | {a['ns'] / a['n'] / 1e3:.1f} | {util * 100:.1f} % | {tf:.0f} | "
-              f"{tf / PEAK_TFLOPS['bf16'] * 100:.1f} % |")
+        a["util"] = a["busy"] / (a["gui"] / 8.0 * 1024.0)
+        a["tflops"] = a["mops"] * 512.0 / (a["ns"] * 1e-9) / 1e12
+        print(f"| {k} | {a['n']} | {a['ns'] / a['n'] / 1e3:.1f} | {a['util'] * 100:.1f} % | "
+              f"{a['tflops']:.0f} | {a['tflops'] / PEAK_TFLOPS['bf16'] * 100:.1f} % |")
+    return agg
 
 
 def main():
