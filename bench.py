@@ -63,6 +63,9 @@ def parse():
     ap.add_argument("--summarize-traffic", metavar="DIR", default=None,
                     help="no GPU work: turn the FETCH_SIZE / WRITE_SIZE counter CSVs of two "
                          "rocprofv3 --pmc runs in DIR into profiles/fc1_wgrad_cfg<N>_traffic.json")
+    ap.add_argument("--summarize-counters", metavar="CSV", default=None,
+                    help="no GPU work: print, per grouped-GEMM kernel, the mean of every "
+                         "counter in a rocprofv3 --pmc CSV per dispatch")
     ap.add_argument("--summarize-mfma", metavar="CSV", default=None,
                     help="no GPU work: print a per-kernel MFMA utilisation table from a "
                          "rocprofv3 --pmc CSV of SQ_VALU_MFMA_BUSY_CYCLES, "
@@ -155,6 +158,47 @@ def summarize_traffic(d, cfg, path=None):
     return out
 
 
+def _gemm_dispatches(path):
+    """Dispatches of the 256 x 256 grouped GEMMs in a counter CSV, keyed by
+    the kernel's role; each with its duration (ns) and its counters."""
+    import re
+    rows = _counter_rows(path)
+    disp = {}
+    for r in rows:
+        e = disp.setdefault(r["Dispatch_Id"], {"name": r["Kernel_Name"], "ns":
+                            int(r["End_Timestamp"]) - int(r["Start_Timestamp"]), "ctr": {}})
+        e["ctr"][r["Counter_Name"]] = e["ctr"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    out = {}
+    for e in disp.values():
+        m = re.search(r"(Prob\w+)<unsigned short, [^<]*Cfg<256, 256[^>]*>(?:, (true|false))?(?:, (\d))?",
+                      e["name"])
+        if not m or "split" not in e["name"]:
+            continue
+        k = {"ProbFC1": "fc1_recompute" if m.group(2) == "true" else "fc1", "ProbFC2": "fc2",
+             "ProbFC2Dgrad": "fc2_dgrad", "ProbFC1Dgrad": "fc1_dgrad",
+             "ProbWgrad": ("fc1_wgrad" if m.group(2) == "true" else "fc2_wgrad")
+             + (", dW accumulated" if m.group(3) == "1" else ", dW written")}[m.group(1)]
+        out.setdefault(k, []).append(e)
+    return out
+
+
+def summarize_counters(path):
+    """Per grouped-GEMM kernel: launches, mean duration and the mean of each
+    counter per dispatch (summed over the counter's instances)."""
+    by = _gemm_dispatches(path)
+    names = sorted({c for es in by.values() for e in es for c in e["ctr"]})
+    print("| kernel | launches | avg us | " + " | ".join(names) + " |")
+    print("|---|---:|---:|" + "---:|" * len(names))
+    res = {}
+    for k, es in sorted(by.items(), key=lambda kv: -sum(e["ns"] for e in kv[1])):
+        n = len(es)
+        mean = {c: sum(e["ctr"].get(c, 0.0) for e in es) / n for c in names}
+        res[k] = {"launches": n, "avg_ns": sum(e["ns"] for e in es) / n, **mean}
+        print(f"| {k} | {n} | {res[k]['avg_ns'] / 1e3:.1f} | "
+              + " | ".join(f"{mean[c]:.4g}" for c in names) + " |")
+    return res
+
+
 def summarize_mfma(path):
     """Per GEMM kernel: MFMA busy share (rocprofv3's MfmaUtil: busy cycles
     summed over the SIMDs / (GUI-active cycles of one XCD x 1024 SIMDs); the
@@ -200,6 +244,9 @@ def main():
         return
     if args.summarize_mfma:
         summarize_mfma(args.summarize_mfma)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters)
         return
     if args.gpus != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
