@@ -76,6 +76,16 @@ constexpr int kMmaPrio = MEMFINE_MMA_PRIO;
 #define MEMFINE_DIRECT_PRIO 1
 #endif
 constexpr int kDirectPrio = MEMFINE_DIRECT_PRIO;
+// Carry each K tile's last MFMA step over the next K step's barrier (see
+// mma_tile_carry) in the direct-copy loops.
+#ifndef MEMFINE_CARRY_STEP
+#define MEMFINE_CARRY_STEP 1
+#endif
+constexpr bool kCarryStep = MEMFINE_CARRY_STEP;
+// s_waitcnt lgkmcnt(0): this wave's LDS reads have returned
+__device__ __forceinline__ void wait_lgkm0() {
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+}
 
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
@@ -450,6 +460,68 @@ __device__ __forceinline__ void mma_tile(const char* As, const char* Bs, Accum<C
     __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
   }
   if constexpr (kPrio > 0) __builtin_amdgcn_s_setprio(0);
+}
+
+// One K tile whose last MFMA step is carried over: its fragments stay in
+// registers (set 1) and its MFMAs are issued by the next call (kCarry)
+// after the next K step's barrier, where they cover that tile's first
+// fragment reads, or by mma_flush after the K loop.
+template <typename T, class C> struct FragSets {
+  typename Mma<T>::Frag a[2][C::MB], b[2][C::NB];
+};
+template <typename T, class C, class OA, class OB, bool kCarry>
+__device__ __forceinline__ void mma_tile_carry(const char* As, const char* Bs, Accum<C>& acc, int wm,
+                                               int wn, int lane, FragSets<T, C>& f) {
+  constexpr int KS = C::KB / (int)sizeof(T) / Mma<T>::kKStep;
+  static_assert(KS % 2 == 0, "the carried step uses fragment set 1");
+  constexpr int kReads = OA::kReadsPerFrag * C::MB + OB::kReadsPerFrag * C::NB;
+  constexpr int kMfma = C::MB * C::NB;
+#pragma clang loop unroll(full)
+  for (int i = 0; i < C::MB; ++i) f.a[0][i] = OA::read(As, wm * C::WTM + i * 32, 0, lane);
+#pragma clang loop unroll(full)
+  for (int j = 0; j < C::NB; ++j) f.b[0][j] = OB::read(Bs, wn * C::WTN + j * 32, 0, lane);
+  if constexpr (kCarry) {
+#pragma clang loop unroll(full)
+    for (int i = 0; i < C::MB; ++i)
+#pragma clang loop unroll(full)
+      for (int j = 0; j < C::NB; ++j) Mma<T>::mma(f.b[1][j], f.a[1][i], acc.v[i][j]);
+  }
+#pragma clang loop unroll(full)
+  for (int kk = 0; kk + 1 < KS; ++kk) {
+    const int cu = kk & 1, nx = cu ^ 1;
+#pragma clang loop unroll(full)
+    for (int i = 0; i < C::MB; ++i) f.a[nx][i] = OA::read(As, wm * C::WTM + i * 32, kk + 1, lane);
+#pragma clang loop unroll(full)
+    for (int j = 0; j < C::NB; ++j) f.b[nx][j] = OB::read(Bs, wn * C::WTN + j * 32, kk + 1, lane);
+#pragma clang loop unroll(full)
+    for (int i = 0; i < C::MB; ++i)
+#pragma clang loop unroll(full)
+      for (int j = 0; j < C::NB; ++j) Mma<T>::mma(f.b[cu][j], f.a[cu][i], acc.v[i][j]);
+  }
+  if constexpr (kSchedHints) {
+    // the carried MFMAs interleaved with step 0's reads, then per step the
+    // MFMAs of step kk interleaved with the reads of step kk + 1
+#pragma clang loop unroll(full)
+    for (int kk = 0; kk < KS; ++kk) {
+      if (kk == 0 && !kCarry) {
+        __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+        continue;
+      }
+#pragma clang loop unroll(full)
+      for (int x = 0; x < kMfma; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (x < kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      if (kReads > kMfma) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kMfma, 0);
+    }
+  }
+}
+template <typename T, class C>
+__device__ __forceinline__ void mma_flush(Accum<C>& acc, const FragSets<T, C>& f) {
+#pragma clang loop unroll(full)
+  for (int i = 0; i < C::MB; ++i)
+#pragma clang loop unroll(full)
+    for (int j = 0; j < C::NB; ++j) Mma<T>::mma(f.b[1][j], f.a[1][i], acc.v[i][j]);
 }
 
 // Accumulator layout.  The MFMA is given the B fragment as its first operand,
@@ -1394,6 +1466,7 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
   const int nk = k_tiles<T, C>(t);
   if constexpr (C::DIRECT) {
     if (!prefetched) issue_prologue<T, C, P>(g, smem, p, t, w, lane);
+    FragSets<T, C> fr;
     for (int kt = 0; kt < nk; ++kt) {
       if constexpr (kDirectPrio == 1) __builtin_amdgcn_s_setprio(2);
       if constexpr (kDeep<C, P>) {
@@ -1408,8 +1481,10 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
       // A bare s_barrier: __syncthreads() would add a memory fence, for which
       // the compiler waits for every copy in flight (vmcnt(0)) and so defeats
       // the deeper stages.  The explicit wait above already makes this wave's
-      // copies of tile kt visible, and every LDS read of the stage the next
-      // copy overwrites has returned (its MFMA has issued).
+      // copies of tile kt visible.  Every LDS read of the stage the next copy
+      // overwrites has returned: its MFMA has issued, or, for the step carried
+      // over the barrier (kCarryStep), the reads are waited for here.
+      if constexpr (kCarryStep) wait_lgkm0();
       __builtin_amdgcn_s_barrier();
       if (kt + C::S - 1 < nk && !(deep && kt + C::S - 1 < 2)) {
         char* st = smem + ((kt + C::S - 1) % C::S) * C::kStage;
@@ -1417,9 +1492,22 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
       }
       if constexpr (kDirectPrio == 1) __builtin_amdgcn_s_setprio(0);
       char* cur = smem + (kt % C::S) * C::kStage;
-      if (active)
-        mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
+      if constexpr (kCarryStep) {
+        if (active) {
+          if (kt == 0)
+            mma_tile_carry<T, C, typename P::OA, typename P::OB, false>(cur, cur + C::BM * C::KB, acc,
+                                                                     wm, wn, lane, fr);
+          else
+            mma_tile_carry<T, C, typename P::OA, typename P::OB, true>(cur, cur + C::BM * C::KB, acc,
+                                                                    wm, wn, lane, fr);
+        }
+      } else {
+        if (active)
+          mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
+      }
     }
+    if constexpr (kCarryStep)
+      if (active && nk > 0) mma_flush<T, C>(acc, fr);
   } else {
     // Register-staged double buffer: the loads of tile kt + 1 are in flight
     // while tile kt is multiplied, then written to the stage that tile kt - 1
