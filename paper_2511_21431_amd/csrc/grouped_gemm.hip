@@ -476,6 +476,8 @@ __device__ __forceinline__ void mma_tile_carry(const char* As, const char* Bs, A
   static_assert(KS % 2 == 0, "the carried step uses fragment set 1");
   constexpr int kReads = OA::kReadsPerFrag * C::MB + OB::kReadsPerFrag * C::NB;
   constexpr int kMfma = C::MB * C::NB;
+  constexpr int kPrio = C::DIRECT ? 0 : kMmaPrio;  // as in mma_tile
+  if constexpr (kPrio > 0) __builtin_amdgcn_s_setprio(kPrio);
 #pragma clang loop unroll(full)
   for (int i = 0; i < C::MB; ++i) f.a[0][i] = OA::read(As, wm * C::WTM + i * 32, 0, lane);
 #pragma clang loop unroll(full)
@@ -515,6 +517,7 @@ __device__ __forceinline__ void mma_tile_carry(const char* As, const char* Bs, A
       if (kReads > kMfma) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kMfma, 0);
     }
   }
+  if constexpr (kPrio > 0) __builtin_amdgcn_s_setprio(0);
 }
 template <typename T, class C>
 __device__ __forceinline__ void mma_flush(Accum<C>& acc, const FragSets<T, C>& f) {
@@ -1518,19 +1521,34 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
       wait_vm<0>();
       p.commit(smem, smem + C::BM * C::KB, w, lane);
     }
+    FragSets<T, C> fr;
     for (int kt = 0; kt < nk; ++kt) {
+      // (the fence of __syncthreads also waits for the carried step's reads)
       __syncthreads();
       char* cur = smem + (kt & 1) * C::kStage;
       char* nxt = smem + ((kt + 1) & 1) * C::kStage;
       const bool more = kt + 1 < nk;
       if (more) p.issue(g, t, kt + 1, nxt, nxt + C::BM * C::KB, w, lane);
-      if (active)
-        mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
+      if constexpr (kCarryStep) {
+        if (active) {
+          if (kt == 0)
+            mma_tile_carry<T, C, typename P::OA, typename P::OB, false>(cur, cur + C::BM * C::KB, acc,
+                                                                     wm, wn, lane, fr);
+          else
+            mma_tile_carry<T, C, typename P::OA, typename P::OB, true>(cur, cur + C::BM * C::KB, acc,
+                                                                    wm, wn, lane, fr);
+        }
+      } else {
+        if (active)
+          mma_tile<T, C, typename P::OA, typename P::OB>(cur, cur + C::BM * C::KB, acc, wm, wn, lane);
+      }
       if (more) {
         wait_vm<0>();
         p.commit(nxt, nxt + C::BM * C::KB, w, lane);
       }
     }
+    if constexpr (kCarryStep)
+      if (active && nk > 0) mma_flush<T, C>(acc, fr);
   }
   next(smem, w, lane);
   char* slab = slab_of<C, kArray>(smem, w);
