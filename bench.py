@@ -7,13 +7,25 @@ expert counts (the paper's "first notification") -> memory-aware chunk plan
 backward (Eq. (7)).  Inputs are synthetic, seeded, and resident in HBM before
 the timed region starts.
 
+The default workload is the largest single-GPU one: the paper's per-GPU
+worst case of e*s*t_k = 32*4096*8 = 1 048 576 token-slots (131072 received
+tokens x top-8, h = 7168, F = 2048, 32 local experts, one expert taking half
+of the slots), with the chunk count the planner picks for an 8 GB activation
+budget.
+
 Prints ONE JSON line (rank 0, N = 1 GPU):
   value        received tokens per second (whole job = one GPU)
-  roofline     the dominant kernel's algorithmic TFLOP/s against the bf16
-               MFMA peak, measured with HIP events inside the timed region
+  roofline     the dominant kernel against its roofline (algorithmic flops
+               or bytes per launch over its mean launch time, HIP events on
+               the launch stream inside the timed region)
+  gemm         every grouped GEMM's algorithmic TFLOP/s and share of the
+               bf16 peak, beside the 60 % target
   cpu_baseline the fp64 oracle on the host cores, on a bounded token sample
   chunks_sweep tokens/s and measured peak activation bytes for every chunk
                count of the workload, beside the memory-model predictions
+  budget_sweep the planner's chunk count per activation budget with the
+               measured peak (workload 5: 4-64 GB; the dense-FFN workload 3,
+               where the backward holds more per slot than Table 2's rows)
 """
 from __future__ import annotations
 
@@ -37,7 +49,10 @@ PEAK_HBM_GBS = 8000.0
 DEFAULT_BUDGET = {1: 64 * 1024, 2: 250 * 10**6, 3: 500 * 10**6, 4: 10**9, 5: 8 * 10**9}
 # activation budgets swept through the planner (workload 5: 4 GB to 64 GB);
 # each budget's C is joined with the measured chunk sweep
-BUDGET_SWEEP = {5: [4 * 10**9, 8 * 10**9, 16 * 10**9, 32 * 10**9, 64 * 10**9]}
+BUDGET_SWEEP = {5: [4 * 10**9, 8 * 10**9, 16 * 10**9, 32 * 10**9, 64 * 10**9],
+                3: [5 * 10**8, 10**9, 13 * 10**8, 2 * 10**9, 25 * 10**8, 4 * 10**9]}
+GEMMS = ("fc1", "fc2", "fc1_recompute", "fc2_dgrad", "fc2_wgrad", "fc1_wgrad", "fc1_dgrad")
+GEMM_TARGET = 0.60   # share of the bf16 MFMA peak the grouped GEMMs aim for
 
 
 def log(msg):
@@ -49,13 +64,15 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, help="workload number (1-5)")
+    ap.add_argument("--config", type=int, default=5, help="workload number (1-5)")
     ap.add_argument("--budget", type=float, default=None, help="activation budget, bytes")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-router", action="store_true",
                     help="skip the router and block measurement")
+    ap.add_argument("--no-budget3", action="store_true",
+                    help="skip the workload-3 activation-budget sweep")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target duration of the oracle sample")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -398,13 +415,25 @@ def main():
             r = by_c.get(C_b, {})
             budget_sweep.append({
                 "budget_bytes": b, "status": mf.memfine_status_str(rc_b), "chunks": C_b,
-                "c_theory": info_b["c_theory"],
+                "c_theory": info_b["c_theory"], "paper_model_chunks": info_b["paper_chunks"],
                 "tokens_per_s": r.get("tokens_per_s"),
                 "peak_activation_bytes": r.get("peak_activation_bytes"),
+                "predicted_bytes_impl": info_b["workspace_bytes"],
                 "predicted_bytes_paper_model": r.get("predicted_bytes_paper_model"),
                 "within_budget": (r["peak_activation_bytes"] <= b) if r else None})
             log(f"[bench] budget {b / 1e9:.0f} GB: C={C_b} (c={info_b['c_theory']}), "
                 f"{r.get('tokens_per_s')} tokens/s, peak {r.get('peak_activation_bytes')} B")
+
+    # ---- the same on the dense-FFN workload 3 (F > h: the backward holds
+    # more bytes per slot than Table 2's rows), each budget's C run once with
+    # the allocator hook
+    budget_sweep3 = None
+    if cfg != 3 and not args.no_budget3 and not args.no_sweep:
+        budget_sweep3 = sweep_budgets(mf, torch, 3)
+
+    # ---- MACT from the model configuration (Eq. (1)-(3), Section 4.2
+    # thresholds) for the paper's Model I, beside the counts-based plan
+    mact = mact_model_plan(mf, int(sum(mf.memfine_count(shape, idx, work))))
 
     # ---- the router in front of the layer: its kernels, and the whole block
     router = None
@@ -437,8 +466,12 @@ def main():
         "step_ms_median": round(step_ms[len(step_ms) // 2], 4),
         "step_ms_min": round(step_ms[0], 4),
         "slots_per_s": round(w.N * args.steps / (t1 - t0), 1),
-        "mfma_util_layer": round(executed_flops / (ms_per_step * 1e-3) / 1e12 / peak, 4),
+        # algorithmic (executed) flops of the step, 22 N h F, over the step
+        # time, as a share of the bf16 peak: not a hardware MFMA counter
+        "layer_flops_frac_of_peak": round(executed_flops / (ms_per_step * 1e-3) / 1e12 / peak, 4),
         "layer_tflops": round(executed_flops / (ms_per_step * 1e-3) / 1e12, 1),
+        "gemm": gemm_table(prof_all, peak),
+        "gemm_target_frac_of_peak": GEMM_TARGET,
         "roofline": {"kernel": dominant, "bound": bound, "achieved": round(achieved, 1),
                      "peak": PEAK_HBM_GBS if bound == "hbm" else peak,
                      "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
@@ -455,10 +488,104 @@ def main():
         "layer_roofline_frac": round(layer_bound_ms(prof_all, peak) / ms_per_step, 4),
         "chunks_sweep": sweep,
         "budget_sweep": budget_sweep,
+        "budget_sweep_workload3": budget_sweep3,
+        "mact_model_plan": mact,
         "router": router,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def gemm_table(prof, peak_tflops):
+    """Each grouped GEMM of one instrumented step: algorithmic TFLOP/s (HIP
+    events around its launches) and its share of the bf16 peak."""
+    out = {}
+    for k in GEMMS:
+        v = prof.get(k)
+        if not v or v["total_ms"] <= 0:
+            continue
+        tf = v["flops"] / (v["total_ms"] * 1e-3) / 1e12
+        out[k] = {"ms": round(v["total_ms"], 4), "tflops": round(tf, 1),
+                  "frac_of_peak": round(tf / peak_tflops, 4)}
+    return out
+
+
+def sweep_budgets(mf, torch, cfg):
+    """The planner's chunk count for each activation budget of BUDGET_SWEEP on
+    workload `cfg`, and one layer step at that count with the allocator hook:
+    the measured peak activation against the budget.  Also the bin that
+    Table 2's bytes per slot alone would give and whether this layer's
+    workspace would have fit it."""
+    import moe_workloads as mw
+    w = mw.WORKLOADS[cfg]
+    shape = mf.make_shape(w.T, w.h, w.F, w.E, w.k, mf.BF16)
+    log(f"[bench] budget sweep, workload {cfg} {w.name}: generating inputs")
+    idx_np, gates_np = mw.make_routing(w, cfg)
+    dev = mw.make_tensors_device(w, cfg, "cuda")
+    idx = torch.from_numpy(idx_np).cuda()
+    gates = torch.from_numpy(gates_np).cuda()
+    Y = torch.empty((w.T, w.h), dtype=torch.bfloat16, device="cuda")
+    dX = torch.empty_like(Y)
+    dW1 = torch.empty((w.E, 2 * w.F, w.h), dtype=torch.float32, device="cuda")
+    dW2 = torch.empty((w.E, w.h, w.F), dtype=torch.float32, device="cuda")
+    dg = torch.empty((w.T, w.k), dtype=torch.float32, device="cuda")
+    work = torch.zeros(w.E + 1, dtype=torch.int32, device="cuda")
+    counts = mf.memfine_count(shape, idx, work)
+    rows = []
+    for b in BUDGET_SWEEP[cfg]:
+        rc, C, info = mf.memfine_plan(shape, counts, b, bins=w.bins)
+        alloc = mf.TorchAllocator()
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        mf.memfine_moe_fwd(shape, C, dev["X"], idx, gates, dev["W1"], dev["W2"], Y, allocator=alloc)
+        mf.memfine_moe_bwd(shape, C, dev["X"], idx, gates, dev["W1"], dev["W2"], dev["dY"], dX,
+                           dW1, dW2, dg, allocator=alloc)
+        torch.cuda.synchronize()
+        peak_b = torch.cuda.max_memory_allocated() - base
+        Cp = info["paper_chunks"]
+        ws_paper = mf.memfine_workspace_bytes(shape, Cp, mf.PASS_BWD)
+        rows.append({"budget_bytes": b, "status": mf.memfine_status_str(rc), "chunks": C,
+                     "c_theory": info["c_theory"], "beta": info["beta"],
+                     "predicted_bytes_impl": info["workspace_bytes"],
+                     "peak_activation_bytes": int(peak_b),
+                     "allocator_high_water_bytes": int(alloc.high_water),
+                     "within_budget": bool(alloc.high_water <= b),
+                     "paper_model_chunks": Cp, "paper_model_beta": info["beta_paper"],
+                     "paper_model_chunks_workspace_bytes": ws_paper,
+                     "paper_model_chunks_within_budget": bool(ws_paper <= b)})
+        log(f"[bench] workload {cfg} budget {b / 1e9:.2f} GB: C={C} (paper model {Cp}), "
+            f"peak {peak_b / 1e9:.3f} GB, within budget: {alloc.high_water <= b}")
+    del dev, Y, dX, dW1, dW2
+    torch.cuda.empty_cache()
+    return {"workload": f"{w.name}: T={w.T}, h={w.h}, F={w.F}, E={w.E}, top-{w.k}", "rows": rows}
+
+
+# Table 3's Model I on the paper's setup (Section 5): 64 GB GPUs, 43.0 GB of
+# static memory (Table 4), p = 4 pipeline stages, full recomputation
+MODEL_I = dict(b=1, s=4096, h=7168, a=128, h_d=128, k_a=128, e_n=256, g_e=2048, t=1, c=1,
+               v=1, p=4, D_t=2, full_recompute=1)
+MODEL_I_GPU = dict(M_gpu=64 * 10**9, alpha=(9, 10), M_sta=43 * 10**9)
+
+
+def mact_model_plan(mf, s_recv):
+    """MACT's threshold table for Model I at every pipeline rank and the bin
+    it selects for this step's received slots (the library's host entry
+    points, Eq. (1)-(3) and Section 4.2)."""
+    bins = (1, 2, 4, 8, 16)
+    m = mf.make_model(**MODEL_I)
+    ranks = []
+    for r in range(MODEL_I["p"]):
+        th = mf.memfine_mact_thresholds(m, r, MODEL_I_GPU["M_gpu"], *MODEL_I_GPU["alpha"],
+                                        MODEL_I_GPU["M_sta"], bins)
+        rc, C = mf.memfine_mact_select(bins, th, s_recv)
+        ranks.append({"r_pp": r, "thresholds": th, "chunks": C,
+                      "status": mf.memfine_status_str(rc)})
+    log(f"[bench] MACT Model I, s''={s_recv}: " + ", ".join(f"rank {x['r_pp']} C={x['chunks']}"
+                                                           for x in ranks))
+    return {"model": "Table 3 Model I (h=7168, g_e=2048, s=4096), 64 GB GPU, alpha=0.9, "
+                     "M_sta=43.0 GB, p=4, full recomputation", "s_recv": s_recv,
+            "bins": list(bins), "ranks": ranks}
 
 
 def layer_bound_ms(prof, peak_tflops):

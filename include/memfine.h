@@ -13,17 +13,16 @@
  * ---------------------------------------
  * - Pointers named d_* are device pointers, h_* host pointers.  Every buffer
  *   is owned by the caller; the library keeps no state between calls except a
- *   lazily created per-process profiling table; for calls made with a NULL
- *   allocator, one workspace block per (device, stream), carved into each
- *   chunk's buffers and reused by the next chunk in stream order (grown from
- *   a per-device stream-ordered pool when a call needs more, never shrunk,
- *   kept until the process ends); one pinned host buffer of 1025 ints per
- *   device for memfine_count; and, only when MEMFINE_STREAMS=1 is set, two
- *   side streams and three events per device (kept until the process ends).
- * - Environment variables MEMFINE_TILE, MEMFINE_RASTER, MEMFINE_SPLIT,
- *   MEMFINE_PAIR and MEMFINE_STREAMS, read at every call, select alternative
- *   GEMM tile shapes, tile orders and launch schedules for measurement; every
- *   setting gives bit-identical results.
+ *   lazily created per-process profiling table; the launch options of
+ *   memfine_set_launch_options (one process-wide setting); for calls made
+ *   with a NULL allocator, one workspace block per (device, stream), carved
+ *   into each chunk's buffers and reused by the next chunk in stream order
+ *   (grown from a per-device stream-ordered pool when a call needs more,
+ *   kept until memfine_workspace_trim or the end of the process: see
+ *   memfine_workspace_held); one pinned host buffer of 1025 ints per device
+ *   for memfine_count; and, only when the side-stream launch option is on,
+ *   two side streams and three events per device (kept until the process
+ *   ends).
  * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *   Device work is enqueued asynchronously on it; only memfine_count and
  *   memfine_profile_end synchronise (with the stream / the recorded events).
@@ -92,7 +91,8 @@ typedef struct memfine_shape {
  * argument of a call is NULL the library takes the chunk's buffers from its
  * cached workspace block for the call's stream (see the conventions above):
  * the block's size is the largest per-chunk workspace asked for on that
- * stream so far, and it stays allocated after the call returns.
+ * stream since it was last trimmed, and it stays allocated after the call
+ * returns (memfine_workspace_held / memfine_workspace_trim).
  */
 typedef struct memfine_allocator {
   void* (*alloc)(size_t bytes, void* stream, void* ctx);
@@ -104,14 +104,44 @@ typedef struct memfine_allocator {
  * MEMFINE_ERR_BUDGET). */
 typedef struct memfine_plan_info {
   int64_t s_recv;        /* s'': received slots, the sum of the counts      */
-  int64_t beta;          /* bytes per received slot used by the plan        */
+  int64_t beta;          /* bytes per received slot used by Eq. (8)         */
   int64_t avail;         /* budget - fixed, the numerator of Eq. (8)        */
   double s_max;          /* Eq. (8): avail / beta (for reporting only)      */
   int64_t c_theory;      /* Eq. (9): ceil(s'' / s'_max); -1 if avail <= 0   */
   int32_t chunks;        /* chosen chunk count (a bin)                      */
-  int32_t fits;          /* 1 if chunks >= c_theory                         */
-  int64_t paper_peak_bytes; /* beta * slots of the largest chunk            */
+  int32_t fits;          /* 1 if the call returned MEMFINE_OK               */
+  int64_t paper_peak_bytes; /* beta_paper * slots of the largest chunk      */
+  int64_t beta_paper;    /* Table 2 rows 11-13: D_t (2h + 2F)               */
+  int64_t beta_impl;     /* this library's backward bytes per slot          */
+  int64_t workspace_bytes; /* memfine_workspace_bytes(chunks, backward)     */
+  int32_t paper_chunks;  /* the bin Eq. (8)/(9) give with beta_paper alone  */
+  int32_t reserved;
 } memfine_plan_info;
+
+/*
+ * GEMM launch options, for measurements and tests; every setting gives
+ * bit-identical results (each output element is one lane's fp32 sum in
+ * increasing K order whatever the tiling).  Process-wide; a layer call reads
+ * them once when it starts.
+ */
+#define MEMFINE_TILE_AUTO    0   /* per problem (the default)                  */
+#define MEMFINE_TILE_128     1   /* 128 x 128 tiles, 4 waves                   */
+#define MEMFINE_TILE_256     2   /* 256 x 256 tiles, 8 waves, direct copies    */
+#define MEMFINE_TILE_256_REG 3   /* 256 x 256 tiles, 8 waves, register-staged  */
+typedef struct memfine_launch_options {
+  int32_t tile;        /* MEMFINE_TILE_*                                       */
+  int32_t raster;      /* -1 per problem; 0 row-major by workgroup id; 1..3
+                          XCD blocks with groups of 4, 8, 16 m-tiles; 4 XCD
+                          blocks row-major                                     */
+  int32_t split_tail;  /* 1: a short last round of a GEMM runs as quarter tiles */
+  int32_t pair;        /* 1: FC1 dgrad and FC1 wgrad in one launch             */
+  int32_t streams;     /* 1: the weight gradients on two side streams          */
+} memfine_launch_options;
+
+/* NULL restores the defaults {AUTO, -1, 1, 0, 0}.  MEMFINE_ERR_INVALID_ARG on
+ * a value out of range (the setting is then unchanged). */
+int memfine_set_launch_options(const memfine_launch_options* opts);
+int memfine_get_launch_options(memfine_launch_options* opts_out);
 
 /*
  * Expert counts over all T tokens: the "first notification" of the paper's
@@ -150,15 +180,23 @@ int memfine_dispatch(const memfine_shape* shape, const int32_t* d_idx, int64_t t
  *   budget_bytes  the numerator of Eq. (8): memory left for this layer's
  *                 chunked MoE activations (alpha*M_GPU - M_sta - non-MoE)
  *   fixed_bytes   subtracted from the budget first (>= 0)
- *   beta_bytes    bytes per received slot; 0 selects the paper's Table 2
- *                 rows 11-13, D_t * (2h + 2F)
+ *   beta_bytes    bytes per received slot, see below
  *   bins, nbins   allowed chunk counts (each >= 1), e.g. {1, 2, 4, 8}
  * Chooses s'' = sum(counts), s'_max = (budget - fixed) / beta (Eq. (8)),
  * c = ceil(s'' / s'_max) (Eq. (9)), then the smallest bin >= c (decided
- * exactly as bin * (budget - fixed) >= s'' * beta).  If no bin is large
- * enough, or budget - fixed <= 0, *chunks_out = the largest bin and the call
- * returns MEMFINE_ERR_BUDGET.  s'' = 0 gives the smallest bin.  `info` may be
- * NULL.
+ * exactly as bin * (budget - fixed) >= s'' * beta).
+ *   beta_bytes > 0: that beta; the paper's model alone decides.
+ *   beta_bytes = 0 (default): beta = max(beta_paper, beta_impl), the larger
+ *     of Table 2 rows 11-13, D_t (2h + 2F), and this library's own backward
+ *     bytes per slot; then, so that Eq. (3) holds for the memory the layer
+ *     really takes, the chosen bin moves up to the next bin while
+ *     memfine_workspace_bytes(bin, backward) > budget - fixed (the rounding
+ *     of the chunk split and the per-chunk metadata are not in Eq. (9)).
+ *     On MEMFINE_OK the chunk's workspace therefore fits the budget.
+ * If no bin is large enough, or budget - fixed <= 0, *chunks_out = the
+ * largest bin and the call returns MEMFINE_ERR_BUDGET.  s'' = 0 gives the
+ * smallest bin.  `info` may be NULL; info->paper_chunks reports the bin that
+ * the paper's beta alone would give.
  */
 int memfine_plan(const memfine_shape* shape, const int64_t* h_counts, int64_t budget_bytes,
                  int64_t fixed_bytes, int64_t beta_bytes, const int32_t* bins, int32_t nbins,
@@ -172,6 +210,29 @@ int memfine_plan(const memfine_shape* shape, const int64_t* h_counts, int64_t bu
  * invalid arguments.
  */
 int64_t memfine_workspace_bytes(const memfine_shape* shape, int32_t chunks, int32_t pass);
+
+/*
+ * The library's cached workspace block for calls with a NULL allocator
+ * (paper Section 4.1: the layer's activation peak is the largest chunk's).
+ * memfine_workspace_held: bytes of the block kept for (the current device,
+ * `stream`); 0 if none.  memfine_workspace_trim: if that block is larger than
+ * keep_bytes, it is released in stream order (after the work enqueued on
+ * `stream` so far) and, when keep_bytes > 0, replaced by a block of
+ * keep_bytes; afterwards the held bytes are at most keep_bytes.  A caller
+ * that raises the chunk count to free memory trims to
+ * memfine_workspace_bytes(new chunks, MEMFINE_PASS_BWD).  Not to be called
+ * while a layer call runs on the same stream from another thread.
+ */
+int memfine_workspace_held(void* stream, int64_t* bytes_out);
+int memfine_workspace_trim(void* stream, int64_t keep_bytes);
+
+/*
+ * High-water mark of the library's per-device stream-ordered pool (the
+ * bytes its blocks held at most at once, on the current device) since the
+ * pool was created or last reset (reset = 1 resets it after reading).  0
+ * before the first call that needed a block.
+ */
+int memfine_pool_high_water(int64_t* bytes_out, int32_t reset);
 
 /* ------------------------------------------------------------------------
  * MACT from the model configuration (paper Section 3 and Section 4.2).

@@ -26,9 +26,10 @@ Passages followed
 Readings (the paper is ambiguous here)
 --------------------------------------
 * s' and s'' count token-slots (rows after dispatch), not distinct tokens.
-* "the large bin that is closest to c" is read as the smallest bin >= c, so
-  that the chosen chunk count keeps the chunk under the budget; when no bin is
-  large enough the largest bin is returned with a budget error.
+* Section 4.2's bin choice after Eq. (9) (a bin near c, on the large side)
+  is read as the smallest bin >= c, so that the chosen chunk count keeps the
+  chunk under the budget; when no bin is large enough the largest bin is
+  returned with a budget error.
 * The planner's budget is the numerator of Eq. (8) (alpha*M_GPU - M_sta -
   the non-MoE activation term), minus an optional fixed allowance, for one
   layer with m_g = t = c = b = 1.
@@ -58,7 +59,9 @@ def _F(x) -> Fraction:
 # --- Eq. (1) ----------------------------------------------------------------
 def static_memory(S_para: Iterable[int], v: int, l: int,
                   D_para: int = 2, D_grad: int = 2, D_opt: int = 4) -> Fraction:
-    """Eq. (1): weights + gradients + four optimizer-state copies."""
+    """Eq. (1): weights + gradients + four optimizer-state copies.  Parity
+    unpinned: the paper prints no per-module weight sizes S_i to check it
+    against, so only its C counterpart is compared with it."""
     S = sum(_F(s) for s in S_para)
     return D_para * v * l * S + D_grad * v * l * S + 4 * D_opt * v * l * S
 

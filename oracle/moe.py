@@ -303,24 +303,42 @@ def moe_dW_expert(X, idx, gates, W1, W2, dY, e: int):
     return dW1, dW2
 
 
-def moe_dW_expert_columns(X, idx, gates, W1, W2, dY, e: int, fs):
+def moe_dW_expert_columns(X, idx, gates, W1, W2, dY, e: int, fs, block: int = 32768):
     """Selected columns f of expert e's weight gradients, each from its
     definition over the expert's slots: rows f and F+f of dW1[e] and column f
     of dW2[e].  Returns (dW1_gate [len(fs), h], dW1_up [len(fs), h],
-    dW2_col [h, len(fs)])."""
+    dW2_col [h, len(fs)]).
+
+    The sum over the expert's slots is taken `block` slots at a time (in
+    ascending slot order), so that at most `block` gathered rows of X and dY
+    are held in fp64 at once: a hot expert of the paper's worst case holds
+    half a million slots."""
     k = idx.shape[1]
     F = W1.shape[1] // 2
     fs = np.asarray(list(fs), dtype=np.int64)
     slots = np.nonzero(np.asarray(idx).reshape(-1) == e)[0]
-    tok = slots // k
-    jj = slots % k
-    x = _f64(X[tok])
-    g = _f64(gates)[tok, jj]
-    dy = _f64(dY[tok])
-    ug = x @ _f64(W1[e][fs]).T                      # [n_e, |fs|]
-    uu = x @ _f64(W1[e][F + fs]).T
-    a = silu(ug) * uu
-    da = g[:, None] * (dy @ _f64(W2[e][:, fs]))     # [n_e, |fs|]
-    du_g = da * uu * silu_grad(ug)
-    du_u = da * silu(ug)
-    return du_g.T @ x, du_u.T @ x, (g[:, None] * dy).T @ a
+    W1g = _f64(W1[e][fs])                           # [|fs|, h]
+    W1u = _f64(W1[e][F + fs])
+    W2c = _f64(W2[e][:, fs])                        # [h, |fs|]
+    h = W1g.shape[1]
+    g1 = np.zeros((len(fs), h))
+    u1 = np.zeros((len(fs), h))
+    c2 = np.zeros((h, len(fs)))
+    gates64 = _f64(gates)
+    for b0 in range(0, len(slots), max(1, int(block))):
+        sl = slots[b0:b0 + block]
+        tok = sl // k
+        jj = sl % k
+        x = _f64(X[tok])
+        g = gates64[tok, jj]
+        dy = _f64(dY[tok])
+        ug = x @ W1g.T                              # [rows, |fs|]
+        uu = x @ W1u.T
+        a = silu(ug) * uu
+        da = g[:, None] * (dy @ W2c)                # [rows, |fs|]
+        du_g = da * uu * silu_grad(ug)
+        du_u = da * silu(ug)
+        g1 += du_g.T @ x
+        u1 += du_u.T @ x
+        c2 += (g[:, None] * dy).T @ a
+    return g1, u1, c2

@@ -49,7 +49,20 @@ class PlanInfo(ctypes.Structure):
     _fields_ = [("s_recv", ctypes.c_int64), ("beta", ctypes.c_int64), ("avail", ctypes.c_int64),
                 ("s_max", ctypes.c_double), ("c_theory", ctypes.c_int64),
                 ("chunks", ctypes.c_int32), ("fits", ctypes.c_int32),
-                ("paper_peak_bytes", ctypes.c_int64)]
+                ("paper_peak_bytes", ctypes.c_int64), ("beta_paper", ctypes.c_int64),
+                ("beta_impl", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
+                ("paper_chunks", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+TILE_AUTO, TILE_128, TILE_256, TILE_256_REG = 0, 1, 2, 3
+
+
+class LaunchOptions(ctypes.Structure):
+    """memfine_launch_options: GEMM tile shape, tile order, split tail, paired
+    FC1 backward launch, side streams (all bit-identical)."""
+    _fields_ = [("tile", ctypes.c_int32), ("raster", ctypes.c_int32),
+                ("split_tail", ctypes.c_int32), ("pair", ctypes.c_int32),
+                ("streams", ctypes.c_int32)]
 
 
 class Model(ctypes.Structure):
@@ -79,6 +92,11 @@ _SIGS = {
     "memfine_plan": (ctypes.c_int, [SHP, I64P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                                     I32P, ctypes.c_int32, I32P, ctypes.POINTER(PlanInfo)]),
     "memfine_workspace_bytes": (ctypes.c_int64, [SHP, ctypes.c_int32, ctypes.c_int32]),
+    "memfine_workspace_held": (ctypes.c_int, [P, I64P]),
+    "memfine_workspace_trim": (ctypes.c_int, [P, ctypes.c_int64]),
+    "memfine_pool_high_water": (ctypes.c_int, [I64P, ctypes.c_int32]),
+    "memfine_set_launch_options": (ctypes.c_int, [ctypes.POINTER(LaunchOptions)]),
+    "memfine_get_launch_options": (ctypes.c_int, [ctypes.POINTER(LaunchOptions)]),
     "memfine_moe_fwd": (ctypes.c_int, [SHP, ctypes.c_int32, P, P, P, P, P, P, ALP, P]),
     "memfine_moe_bwd": (ctypes.c_int, [SHP, ctypes.c_int32, P, P, P, P, P, P, P, P, P, P,
                                        ctypes.c_int32, ALP, P]),
@@ -165,7 +183,13 @@ def _stream(stream) -> ctypes.c_void_p:
 
 class TorchAllocator:
     """Serves the layer's per-chunk buffers from torch's caching allocator,
-    so that torch.cuda.max_memory_allocated sees the layer's true peak."""
+    so that torch.cuda.max_memory_allocated sees the layer's true peak.
+
+    The library asks for and hands back each buffer in order on the stream of
+    its call: a buffer is allocated on that stream (torch then reuses it only
+    in that stream's order), and released with record_stream on it, so torch
+    never hands the memory to other work before the library's kernels that
+    use it have run."""
 
     def __init__(self, device=None):
         torch = _torch()
@@ -179,12 +203,22 @@ class TorchAllocator:
         self._release = RELEASE_FN(self._do_release)
         self.struct = Allocator(self._alloc, self._release, None)
 
+    def _stream(self, stream):
+        """The torch stream object for the library's stream handle."""
+        torch = _torch()
+        ptr = int(stream or 0)
+        for cand in (torch.cuda.current_stream(self.device), torch.cuda.default_stream(self.device)):
+            if cand.cuda_stream == ptr:
+                return cand
+        return torch.cuda.ExternalStream(ptr, device=self.device)
+
     def _do_alloc(self, nbytes, stream, ctx):
         torch = _torch()
         self.calls += 1
         if self.fail_at is not None and self.calls >= self.fail_at:
             return None
-        t = torch.empty(int(nbytes), dtype=torch.uint8, device=self.device)
+        with torch.cuda.stream(self._stream(stream)):
+            t = torch.empty(int(nbytes), dtype=torch.uint8, device=self.device)
         p = t.data_ptr()
         self.live[p] = t
         self.live_bytes += int(nbytes)
@@ -192,7 +226,9 @@ class TorchAllocator:
         return p
 
     def _do_release(self, ptr, nbytes, stream, ctx):
-        if self.live.pop(int(ptr), None) is not None:
+        t = self.live.pop(int(ptr), None)
+        if t is not None:
+            t.record_stream(self._stream(stream))
             self.live_bytes -= int(nbytes)
 
 
@@ -304,6 +340,38 @@ def memfine_workspace_bytes(shape: Shape, chunks: int, pass_: int) -> int:
     if v < 0:
         raise MemfineError(int(v), "memfine_workspace_bytes")
     return int(v)
+
+
+def memfine_workspace_held(stream=None) -> int:
+    """Bytes of the library's cached workspace block for the stream."""
+    out = ctypes.c_int64(0)
+    _check(lib().memfine_workspace_held(_stream(stream), ctypes.byref(out)),
+           "memfine_workspace_held")
+    return int(out.value)
+
+
+def memfine_workspace_trim(keep_bytes: int = 0, stream=None) -> None:
+    _check(lib().memfine_workspace_trim(_stream(stream), int(keep_bytes)), "memfine_workspace_trim")
+
+
+def memfine_pool_high_water(reset: bool = False) -> int:
+    out = ctypes.c_int64(0)
+    _check(lib().memfine_pool_high_water(ctypes.byref(out), 1 if reset else 0),
+           "memfine_pool_high_water")
+    return int(out.value)
+
+
+def memfine_set_launch_options(tile: int = TILE_AUTO, raster: int = -1, split_tail: bool = True,
+                               pair: bool = False, streams: bool = False) -> None:
+    o = LaunchOptions(int(tile), int(raster), int(bool(split_tail)), int(bool(pair)),
+                      int(bool(streams)))
+    _check(lib().memfine_set_launch_options(ctypes.byref(o)), "memfine_set_launch_options")
+
+
+def memfine_get_launch_options() -> Dict[str, int]:
+    o = LaunchOptions()
+    _check(lib().memfine_get_launch_options(ctypes.byref(o)), "memfine_get_launch_options")
+    return {f: getattr(o, f) for f, _ in LaunchOptions._fields_}
 
 
 def memfine_moe_fwd(shape: Shape, chunks: int, X, idx, gates, W1, W2, Y, allocator=None,

@@ -255,37 +255,16 @@ ChunkBuffers carve(void* base, const Layout& L) {
   return c;
 }
 
-// Launch options for measurements and tests, read from the environment at
-// every call (a getenv per launch), so that one process can switch them.
-int env_int(const char* name, int dflt) {
-  const char* e = getenv(name);
-  return e ? atoi(e) : dflt;
+// Launch options (memfine_set_launch_options): one process-wide setting,
+// copied under a lock at the start of every layer call, so that a call never
+// sees a half-written update.  The defaults are the measured-best choices.
+std::mutex g_opts_mu;
+memfine_launch_options g_opts = {MEMFINE_TILE_AUTO, -1, 1, 0, 0};
+
+memfine_launch_options launch_options() {
+  std::lock_guard<std::mutex> lk(g_opts_mu);
+  return g_opts;
 }
-
-// MEMFINE_TILE pins the bf16 GEMM tile shape (1..11, see launch_auto in
-// grouped_gemm.hip; 128 = 1, 256 = 2).
-int tile_override() {
-  const int t = env_int("MEMFINE_TILE", 0);
-  return t == 128 ? 1 : t == 256 ? 2 : (t >= 1 && t <= 11) ? t : 0;
-}
-
-// MEMFINE_RASTER selects the GEMM tile traversal for every GEMM (0..4; 0
-// row-major by workgroup id, 1..3 XCD blocks with groups of 4, 8, 16
-// m-tiles, 4 XCD blocks row-major).  Unset (-1), each problem takes its own
-// measured best: XCD blocks for the row-grouped GEMMs, the round-robin
-// expert order for the weight gradients.
-int raster_mode() {
-  const int t = env_int("MEMFINE_RASTER", -1);
-  return (t >= -1 && t <= 4) ? t : -1;
-}
-
-// MEMFINE_PAIR=1 runs the FC1 dgrad and FC1 wgrad of the backward in one
-// launch (default 0: two launches).
-bool pair_launches() { return env_int("MEMFINE_PAIR", 0) == 1; }
-
-// MEMFINE_SPLIT=0 keeps the last, partial round of a GEMM in full-size tiles
-// (default 1: quarter tiles when it is at most half full).
-int split_tail() { return env_int("MEMFINE_SPLIT", 1) == 0 ? 0 : 1; }
 
 // Compute units of the current device (cached per device id).
 int device_cus() {
@@ -305,12 +284,6 @@ int device_cus() {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? MEMFINE_OK : MEMFINE_ERR_HIP; }
 
-// MEMFINE_STREAMS=1 runs the backward's two weight gradients on side
-// streams beside the FC1 dgrad (default 0: the three one after another on
-// the caller's stream).  Measured on MI355X: 4 % faster on the 7168-wide
-// 32-expert workload at C = 2, 1 % slower on the 2048-wide one, equal at
-// C = 1; the concurrent launches mostly split the CUs between them.
-bool overlap_streams() { return env_int("MEMFINE_STREAMS", 0) == 1; }
 
 // Two side streams per device (non-blocking, default priority) and the
 // events of one fork/join.  `mu` is held from the fork to the join, so that
@@ -345,7 +318,8 @@ SideStreams* side_streams() {
   return &c;
 }
 
-GemmArgs gemm_args(const memfine_shape& s, int64_t n, const ChunkBuffers& c) {
+GemmArgs gemm_args(const memfine_shape& s, int64_t n, const ChunkBuffers& c,
+                   const memfine_launch_options& o) {
   GemmArgs g = {};
   g.dtype = s.dtype;
   g.n = (int)n;
@@ -364,11 +338,37 @@ GemmArgs gemm_args(const memfine_shape& s, int64_t n, const ChunkBuffers& c) {
   g.dgp = c.dgp;
   g.P = dgate_partials(s.F);
   g.T_h_bytes = s.T * (int64_t)s.h * elem_bytes(s);
-  g.tile_override = tile_override();
-  g.raster = raster_mode();
+  g.tile_override = o.tile;
+  g.raster = o.raster;
   g.cus = device_cus();
-  g.split_tail = split_tail();
+  g.split_tail = o.split_tail;
   return g;
+}
+
+// This library's backward bytes per slot, an upper bound of the slope of
+// its per-chunk workspace in the chunk's slots: the intermediates u, g*a
+// and the input gradient (es (3F + h)), the gate-gradient partials, the
+// four per-slot routing tables, and the per-block expert counts.
+int64_t beta_impl(const memfine_shape& s) {
+  return elem_bytes(s) * (3 * (int64_t)s.F + s.h) + 4 * (int64_t)dgate_partials(s.F) + 16 +
+         (s.E + 31) / 32;
+}
+
+// Smallest bin b with b * avail >= num (bin b splits the slots into b chunks
+// of at most s''/b), or -1.
+int32_t smallest_bin_admitting(const int32_t* bins, int nbins, int64_t avail, __int128 num) {
+  int32_t best = INT32_MAX;
+  for (int i = 0; i < nbins; ++i)
+    if ((__int128)bins[i] * avail >= num) best = std::min(best, bins[i]);
+  return best == INT32_MAX ? -1 : best;
+}
+
+// Smallest bin larger than b, or -1.
+int32_t next_bin_above(const int32_t* bins, int nbins, int32_t b) {
+  int32_t best = INT32_MAX;
+  for (int i = 0; i < nbins; ++i)
+    if (bins[i] > b) best = std::min(best, bins[i]);
+  return best == INT32_MAX ? -1 : best;
 }
 
 // Algorithmic work of one launch, for the timing table.
@@ -401,10 +401,9 @@ int memfine_plan(const memfine_shape* shape, const int64_t* h_counts, int64_t bu
   if (rc) return rc;
   if (!h_counts || !bins || nbins < 1 || !chunks_out || fixed_bytes < 0 || beta_bytes < 0)
     return MEMFINE_ERR_INVALID_ARG;
-  int32_t bmin = INT32_MAX, bmax = 0;
+  int32_t bmax = 0;
   for (int i = 0; i < nbins; ++i) {
     if (bins[i] < 1) return MEMFINE_ERR_INVALID_ARG;
-    bmin = std::min(bmin, bins[i]);
     bmax = std::max(bmax, bins[i]);
   }
   __int128 s2 = 0;
@@ -413,26 +412,29 @@ int memfine_plan(const memfine_shape* shape, const int64_t* h_counts, int64_t bu
     s2 += h_counts[e];
   }
   // Table 2 rows 11-13: D_t (h + 2 g_e + h) bytes per received slot
-  const int64_t beta = beta_bytes > 0 ? beta_bytes : elem_bytes(*shape) * (2 * (int64_t)shape->h + 2 * (int64_t)shape->F);
+  const int64_t beta_paper = elem_bytes(*shape) * (2 * (int64_t)shape->h + 2 * (int64_t)shape->F);
+  const int64_t b_impl = beta_impl(*shape);
+  const bool impl_check = beta_bytes == 0;
+  const int64_t beta = beta_bytes > 0 ? beta_bytes : std::max(beta_paper, b_impl);
   const int64_t avail = budget_bytes - fixed_bytes;
-  int32_t chosen = bmax;
   int64_t c_theory = -1;
-  bool fits = false;
+  int32_t chosen = -1;
+  int32_t paper_chosen = -1;
   if (avail > 0) {
     // Eq. (9): c = ceil(s'' / s'_max) = ceil(s'' * beta / avail)
     const __int128 num = s2 * (__int128)beta;
     const __int128 c = (num + avail - 1) / avail;
     c_theory = c > (__int128)INT64_MAX ? INT64_MAX : (int64_t)c;
-    // smallest bin b with b * avail >= s'' * beta
-    int32_t best = INT32_MAX;
-    for (int i = 0; i < nbins; ++i)
-      if ((__int128)bins[i] * avail >= num) best = std::min(best, bins[i]);
-    if (best != INT32_MAX) {
-      chosen = best;
-      fits = true;
-    }
+    chosen = smallest_bin_admitting(bins, nbins, avail, num);
+    paper_chosen = smallest_bin_admitting(bins, nbins, avail, s2 * (__int128)beta_paper);
+    // Eq. (3) on the memory this library really takes: the next larger bin
+    // while the chunk's workspace exceeds what is available
+    while (impl_check && chosen > 0 &&
+           memfine_workspace_bytes(shape, chosen, MEMFINE_PASS_BWD) > avail)
+      chosen = next_bin_above(bins, nbins, chosen);
   }
-  (void)bmin;
+  const bool fits = chosen > 0;
+  if (!fits) chosen = bmax;
   *chunks_out = chosen;
   if (info) {
     info->s_recv = (int64_t)s2;
@@ -442,9 +444,90 @@ int memfine_plan(const memfine_shape* shape, const int64_t* h_counts, int64_t bu
     info->c_theory = c_theory;
     info->chunks = chosen;
     info->fits = fits ? 1 : 0;
-    info->paper_peak_bytes = beta * max_chunk_tokens(shape->T, chosen) * shape->k;
+    info->paper_peak_bytes = beta_paper * max_chunk_tokens(shape->T, chosen) * shape->k;
+    info->beta_paper = beta_paper;
+    info->beta_impl = b_impl;
+    info->workspace_bytes = memfine_workspace_bytes(shape, chosen, MEMFINE_PASS_BWD);
+    info->paper_chunks = paper_chosen > 0 ? paper_chosen : bmax;
+    info->reserved = 0;
   }
   return fits ? MEMFINE_OK : MEMFINE_ERR_BUDGET;
+}
+
+int memfine_set_launch_options(const memfine_launch_options* opts) {
+  memfine_launch_options o = {MEMFINE_TILE_AUTO, -1, 1, 0, 0};
+  if (opts) {
+    if (opts->tile < MEMFINE_TILE_AUTO || opts->tile > MEMFINE_TILE_256_REG ||
+        opts->raster < -1 || opts->raster > 4 || (opts->split_tail != 0 && opts->split_tail != 1) ||
+        (opts->pair != 0 && opts->pair != 1) || (opts->streams != 0 && opts->streams != 1))
+      return MEMFINE_ERR_INVALID_ARG;
+    o = *opts;
+  }
+  std::lock_guard<std::mutex> lk(g_opts_mu);
+  g_opts = o;
+  return MEMFINE_OK;
+}
+
+int memfine_get_launch_options(memfine_launch_options* opts_out) {
+  if (!opts_out) return MEMFINE_ERR_INVALID_ARG;
+  *opts_out = launch_options();
+  return MEMFINE_OK;
+}
+
+int memfine_workspace_held(void* stream, int64_t* bytes_out) {
+  if (!bytes_out) return MEMFINE_ERR_INVALID_ARG;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MEMFINE_ERR_HIP;
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  auto it = g_ws.find({dev, (hipStream_t)stream});
+  *bytes_out = it == g_ws.end() ? 0 : (int64_t)it->second.bytes;
+  return MEMFINE_OK;
+}
+
+int memfine_workspace_trim(void* stream, int64_t keep_bytes) {
+  if (keep_bytes < 0) return MEMFINE_ERR_INVALID_ARG;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MEMFINE_ERR_HIP;
+  hipStream_t s = (hipStream_t)stream;
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  auto it = g_ws.find({dev, s});
+  if (it == g_ws.end()) return MEMFINE_OK;
+  WsBlock& b = it->second;
+  if (b.busy) return MEMFINE_ERR_INVALID_ARG;  // a call on this stream is enqueuing
+  if ((int64_t)b.bytes <= keep_bytes) return MEMFINE_OK;
+  if (b.p && hipFreeAsync(b.p, s) != hipSuccess) return MEMFINE_ERR_HIP;
+  b.p = nullptr;
+  b.bytes = 0;
+  if (keep_bytes > 0) {
+    b.p = pool_alloc((size_t)keep_bytes, s);
+    if (!b.p) return MEMFINE_ERR_OOM;
+    b.bytes = (size_t)keep_bytes;
+  }
+  return MEMFINE_OK;
+}
+
+int memfine_pool_high_water(int64_t* bytes_out, int32_t reset) {
+  if (!bytes_out || (reset != 0 && reset != 1)) return MEMFINE_ERR_INVALID_ARG;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MEMFINE_ERR_HIP;
+  hipMemPool_t pool = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_pool_mu);
+    auto it = g_pools.find(dev);
+    if (it != g_pools.end()) pool = it->second;
+  }
+  *bytes_out = 0;
+  if (!pool) return MEMFINE_OK;
+  uint64_t v = 0;
+  if (hipMemPoolGetAttribute(pool, hipMemPoolAttrUsedMemHigh, &v) != hipSuccess)
+    return MEMFINE_ERR_HIP;
+  *bytes_out = (int64_t)v;
+  if (reset) {
+    uint64_t zero = 0;
+    if (hipMemPoolSetAttribute(pool, hipMemPoolAttrUsedMemHigh, &zero) != hipSuccess)
+      return MEMFINE_ERR_HIP;
+  }
+  return MEMFINE_OK;
 }
 
 int64_t memfine_workspace_bytes(const memfine_shape* shape, int32_t chunks, int32_t pass) {
@@ -536,6 +619,7 @@ int memfine_moe_fwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
   hipStream_t s = (hipStream_t)stream;
   const int64_t C = std::min<int64_t>(chunks, S.T);
   const double es = (double)elem_bytes(S);
+  const memfine_launch_options opt = launch_options();
   for (int64_t i = 0; i < C; ++i) {
     const int64_t t0 = i * S.T / C, t1 = (i + 1) * S.T / C;
     const int64_t tokens = t1 - t0, n = tokens * S.k;
@@ -545,7 +629,7 @@ int memfine_moe_fwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
     void* ws = ws_alloc(alloc, (size_t)L.total, s);
     if (!ws) return MEMFINE_ERR_OOM;
     const ChunkBuffers cb = carve(ws, L);
-    GemmArgs g = gemm_args(S, n, cb);
+    GemmArgs g = gemm_args(S, n, cb, opt);
     g.X = d_X;
     g.W1 = d_W1;
     g.W2 = d_W2;
@@ -600,6 +684,7 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
     return hip_status(err);
   }
   const int64_t C = std::min<int64_t>(chunks, S.T);
+  const memfine_launch_options opt = launch_options();
   bool first = true;
   for (int64_t i = 0; i < C; ++i) {
     const int64_t t0 = i * S.T / C, t1 = (i + 1) * S.T / C;
@@ -610,7 +695,7 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
     void* ws = ws_alloc(alloc, (size_t)L.total, s);
     if (!ws) return MEMFINE_ERR_OOM;
     const ChunkBuffers cb = carve(ws, L);
-    GemmArgs g = gemm_args(S, n, cb);
+    GemmArgs g = gemm_args(S, n, cb, opt);
     g.X = d_X;
     g.dY = d_dY;
     g.W1 = d_W1;
@@ -640,7 +725,7 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
       KernelTimer kt(MEMFINE_K_FC1_RECOMP, s, w_rec.flops, w_rec.bytes);
       err = launch_fc1_recompute(g, s);
     }
-    SideStreams* ss = (!pair_launches() && overlap_streams()) ? side_streams() : nullptr;
+    SideStreams* ss = (!opt.pair && opt.streams) ? side_streams() : nullptr;
     if (ss) {
       // The two weight gradients and the FC1 dgrad read what the recompute
       // wrote and write disjoint outputs (dW1, dW2, the chunk's dX rows).
@@ -690,7 +775,7 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
         gw.tile_ctr = cb.ctr + 1;
         err = launch_fc2_wgrad(gw, s);
       }
-      if (pair_launches()) {
+      if (opt.pair) {
         if (err == hipSuccess) {
           KernelTimer kt(MEMFINE_K_FC1_BWD, s, w_fc1d.flops + w_fc1w.flops,
                          w_fc1d.bytes + w_fc1w.bytes);

@@ -123,7 +123,6 @@ template <int BM_, int BN_, int WM_, int WN_, int S_, int KB_ = 128, int DIRECT_
     }
   }
 };
-using Big = Cfg<256, 256, 2, 2, 2>;
 using Small = Cfg<128, 128, 2, 2, 2>;
 
 // Epilogue staging.  Straight from the accumulators, a 16-byte store
@@ -1671,16 +1670,24 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
       }
     }
   } else if (kDynamic<C, P> && g.tile_ctr != nullptr) {
-    int32_t& s_next = *reinterpret_cast<int32_t*>(smem + C::kLds);
+    // Three LDS words: slot 2 for grab(), slots 0 and 1 for the tile index
+    // fetched ahead, alternating from one tile to the next.  A wave reads
+    // slot p after the barrier that follows thread 0's write; thread 0 writes
+    // slot p again two tiles later, after it has passed the next tile's
+    // barrier, which every wave reaches only after its read - even when the
+    // tile in between has no K steps (an expert without rows) and so no K-loop
+    // barrier.
+    int32_t* s_next = reinterpret_cast<int32_t*>(smem + C::kLds);
     // thread 0 takes a tile index; every wave reads it after a barrier (and
     // again before thread 0 may overwrite it)
     auto grab = [&]() {
-      if (threadIdx.x == 0) s_next = atomicAdd(g.tile_ctr, 1);
+      if (threadIdx.x == 0) s_next[2] = atomicAdd(g.tile_ctr, 1);
       __syncthreads();
-      const int v = __builtin_amdgcn_readfirstlane(s_next);  // uniform: scalar tile state
+      const int v = __builtin_amdgcn_readfirstlane(s_next[2]);  // uniform: scalar tile state
       __syncthreads();
       return v;
     };
+    int par = 0;
     P p;
     Tile t;
     int v = grab();
@@ -1709,9 +1716,9 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
       int vn = nmain;
       bool okn = false;
       run_located<T, C, P>(g, smem, p, t, pre, [&](char* sm, int w, int lane) {
-        if (threadIdx.x == 0) s_next = ahead;
+        if (threadIdx.x == 0) s_next[par] = ahead;
         __syncthreads();  // s_next is visible; every wave is past its last MFMA
-        vn = __builtin_amdgcn_readfirstlane(s_next);
+        vn = __builtin_amdgcn_readfirstlane(s_next[par]);
         okn = vn < nmain && pn.locate(g, tn, vn, nmain);
         if (okn) {
           pn.init(g, tn, w, lane);
@@ -1725,6 +1732,7 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
       }
       v = vn;
       pre = okn;
+      par ^= 1;
       // without a prefetched tile, the grab in the locate loop above (or the
       // quarter-tile barrier below) separates this tile's LDS use from the
       // next one's, and lets every wave read s_next before it changes
@@ -1826,15 +1834,8 @@ inline double rounds(int tiles, int per_cu) {
 
 using Big8 = Cfg<256, 256, 2, 4, 2>;        // 8 waves of 128 x 64
 using Big8R = Cfg<256, 256, 2, 4, 2, 128, 0>;  // Big8 with register-staged copies
-using Big8RA = Cfg<256, 256, 2, 4, 2, 128, 2>; // A staged, B direct
-using Big8RB = Cfg<256, 256, 2, 4, 2, 128, 1>; // A direct, B staged
-using BigR = Cfg<256, 256, 2, 2, 2, 128, 0>;   // Big with register-staged copies
 using Quarter8 = Cfg<128, 128, 4, 2, 2>;        // quarter tiles of Big8 (8 waves of 32 x 64)
 using Quarter8R = Cfg<128, 128, 4, 2, 2, 128, 0>;
-using Big8S4 = Cfg<256, 256, 2, 4, 4, 64>;  // half-depth K tiles, 4 stages
-using Big8S5 = Cfg<256, 256, 2, 4, 5, 64>;  // half-depth K tiles, 5 stages
-using SmallS4 = Cfg<128, 128, 2, 2, 4, 64>;
-using SmallS3 = Cfg<128, 128, 2, 2, 3, 64>;
 
 template <typename T, class C> using FC1Fwd = ProbFC1<T, C, false>;
 template <typename T, class C> using FC1Bwd = ProbFC1<T, C, true>;
@@ -1884,18 +1885,10 @@ hipError_t launch_auto(const GemmArgs& g_in, hipStream_t s) {
   GemmArgs g = g_in;
   if (g.raster < 0) g.raster = PT<float, Big8>::kRaster;
   if (g.dtype != 0) return launch_cfg<PT, Small>(g, s);
-  switch (g.tile_override) {
+  switch (g.tile_override) {  // memfine_launch_options.tile
     case 1: return launch_cfg<PT, Small>(g, s);
-    case 2: return launch_cfg<PT, Big>(g, s);
-    case 3: return launch_cfg<PT, Big8>(g, s);
-    case 4: return launch_cfg<PT, Big8S4>(g, s);
-    case 5: return launch_cfg<PT, Big8S5>(g, s);
-    case 6: return launch_cfg<PT, SmallS4>(g, s);
-    case 7: return launch_cfg<PT, SmallS3>(g, s);
-    case 8: return launch_cfg<PT, Big8R>(g, s);
-    case 9: return launch_cfg<PT, BigR>(g, s);
-    case 10: return launch_cfg<PT, Big8RA>(g, s);
-    case 11: return launch_cfg<PT, Big8RB>(g, s);
+    case 2: return launch_cfg<PT, Big8>(g, s);
+    case 3: return launch_cfg<PT, Big8R>(g, s);
     default: break;
   }
   if (PT<float, Big8>::grid(g) >= 128) {

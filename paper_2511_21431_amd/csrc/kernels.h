@@ -71,7 +71,7 @@ struct GemmArgs {
   float* dW2;        // [E, h, F]
   int accumulate;    // wgrad: 1 = add into dW, 0 = overwrite
   int64_t T_h_bytes; // bytes of X (and of dY): T * h * element size
-  int tile_override; // 0: choose the tile shape per problem; else a fixed shape
+  int tile_override; // 0: per problem; 1: 128 x 128; 2: 256 x 256 direct; 3: 256 x 256 staged
   int raster;        // tile order: -1 per problem; 0 row-major; 1..3 XCD blocks, groups of 4/8/16 m-tiles; 4 XCD blocks, row-major
   int cus;           // compute units of the device
   int split_tail;    // 1: row-grouped GEMMs run a short last round as quarter tiles

@@ -31,6 +31,23 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(_lib._SIGS), "binding and header disagree"
 
 
+def test_launch_options_roundtrip_and_validation():
+    L = _lib.lib()
+    mf.memfine_set_launch_options()
+    assert mf.memfine_get_launch_options() == {"tile": 0, "raster": -1, "split_tail": 1,
+                                               "pair": 0, "streams": 0}
+    mf.memfine_set_launch_options(tile=mf.TILE_256_REG, raster=3, split_tail=False, pair=True)
+    assert mf.memfine_get_launch_options() == {"tile": 3, "raster": 3, "split_tail": 0,
+                                               "pair": 1, "streams": 0}
+    for bad in (dict(tile=4), dict(tile=-1), dict(raster=5), dict(raster=-2)):
+        with pytest.raises(mf.MemfineError):
+            mf.memfine_set_launch_options(**bad)
+    assert mf.memfine_get_launch_options()["tile"] == 3       # unchanged by the rejected calls
+    assert L.memfine_set_launch_options(None) == 0
+    assert mf.memfine_get_launch_options()["tile"] == 0
+    assert L.memfine_get_launch_options(None) == -1
+
+
 def test_status_strings():
     for code in (0, -1, -2, -3, -4, -5):
         assert mf.memfine_status_str(code)
@@ -63,7 +80,9 @@ def test_plan_matches_oracle_randomised():
         fixed = rng.choice([0, 0, rng.randint(0, 10**9)])
         bins = sorted(rng.sample([1, 2, 3, 4, 6, 8, 16], rng.randint(1, 4)))
         shape = mf.make_shape(T, h, F, E, k, dtype)
-        rc, C, info = mf.memfine_plan(shape, counts, budget, bins=bins, fixed_bytes=fixed)
+        # the paper's model alone: beta = Table 2 rows 11-13
+        rc, C, info = mf.memfine_plan(shape, counts, budget, bins=bins, fixed_bytes=fixed,
+                                      beta_bytes=beta)
         ref = mm.plan(counts, budget, beta, bins=bins, fixed=fixed)
         assert C == ref["C"], (budget, fixed, s2, bins, ref)
         assert (rc == 0) == ref["ok"]
@@ -72,6 +91,45 @@ def test_plan_matches_oracle_randomised():
             assert info["c_theory"] == ref["c_theory"]
         else:
             assert info["c_theory"] == -1
+
+
+def test_plan_default_keeps_eq3_for_the_implementation():
+    """Default beta: max(Table 2's, the library's own) and the workspace check.
+    On the dense-FFN shape (F > h: the backward holds more per slot than
+    Table 2's rows) every budget the planner accepts holds the chunk's whole
+    workspace, the chosen bin is the smallest such bin at or above Eq. (9)'s
+    c, and the paper-model bin is reported beside it (Eq. (3), Eq. (8)/(9))."""
+    import moe_workloads as mw
+    w = mw.WORKLOADS[3]
+    idx, _ = mw.make_routing(w, 3)
+    counts = np.bincount(idx.reshape(-1), minlength=w.E)
+    shape = mf.make_shape(w.T, w.h, w.F, w.E, w.k, mf.BF16)
+    beta_paper = 2 * (2 * w.h + 2 * w.F)
+    bins = (1, 2, 4, 8)
+    ws = {b: mf.memfine_workspace_bytes(shape, b, mf.PASS_BWD) for b in bins}
+    rng = np.random.default_rng(7)
+    budgets = sorted(set(np.linspace(0.30e9, 3.15e9, 3000).astype(np.int64).tolist()
+                         + [ws[b] + d for b in bins for d in (-1, 0, 1)]
+                         + rng.integers(10**8, 4 * 10**9, 1000).tolist()))
+    n_ok = n_paper_over = 0
+    for budget in budgets:
+        rc, C, info = mf.memfine_plan(shape, counts, budget, bins=bins)
+        assert info["beta_paper"] == beta_paper and info["beta_impl"] > beta_paper
+        assert info["beta"] == info["beta_impl"]
+        assert info["workspace_bytes"] == ws[C]
+        c = info["c_theory"]
+        feasible = [b for b in bins if b >= c and ws[b] <= budget]
+        if rc == 0:
+            n_ok += 1
+            assert ws[C] <= budget, (budget, C, ws[C])
+            assert C == min(feasible), (budget, C, feasible)
+        else:
+            assert rc == _lib.ERR_BUDGET and not feasible and C == max(bins)
+        ref = mm.plan(counts, budget, beta_paper, bins=bins)
+        assert info["paper_chunks"] == ref["C"]
+        if ref["ok"] and ws[ref["C"]] > budget:
+            n_paper_over += 1           # where Table 2's beta alone would overshoot
+    assert n_ok > 1000 and n_paper_over > 100
 
 
 def test_plan_handworked_config5():

@@ -6,8 +6,8 @@ order over the chip (XCD blocks, row-major), the persistent or one-tile-per-
 workgroup launch, the quarter-tile tail, the paired dgrad/wgrad launch or
 the side-stream schedule.  So all of them must give bit-identical outputs
 and gradients; the default configuration is checked against the oracle in
-test_gpu_parity.py.  The options are environment variables the library
-reads at every call.
+test_gpu_parity.py.  The options are set through memfine_set_launch_options
+(a layer call reads them once when it starts).
 """
 import numpy as np
 import pytest
@@ -22,11 +22,15 @@ pytestmark = pytest.mark.gpu
 W_BIG = mw.scaled(mw.WORKLOADS[2], T=4096, h=512, F=1024, E=8)
 W_F32 = mw.WORKLOADS[1]
 
-CONFIGS = ([{"MEMFINE_RASTER": str(r)} for r in range(5)]
-           + [{"MEMFINE_TILE": str(t)} for t in range(1, 12)]
-           + [{"MEMFINE_SPLIT": "0"}, {"MEMFINE_PAIR": "1"}, {"MEMFINE_STREAMS": "1"},
-              {"MEMFINE_SPLIT": "0", "MEMFINE_RASTER": "2"}])
-KEYS = ("MEMFINE_RASTER", "MEMFINE_TILE", "MEMFINE_SPLIT", "MEMFINE_PAIR", "MEMFINE_STREAMS")
+# memfine_set_launch_options keyword arguments
+CONFIGS = ([{"raster": r} for r in range(5)]
+           + [{"tile": t} for t in (1, 2, 3)]
+           + [{"split_tail": False}, {"pair": True}, {"streams": True},
+              {"split_tail": False, "raster": 2}, {"tile": 3, "raster": 0}])
+
+
+def _ids(c):
+    return ",".join(f"{k}={v}" for k, v in c.items())
 
 
 @pytest.fixture(scope="module")
@@ -48,11 +52,11 @@ def _run(w, dev, C):
 _cache = {}
 
 
-def _reference(w, seed, C, monkeypatch):
+def _reference(w, seed, C):
     key = (w.name, seed, C)
     if key not in _cache:
-        for k in KEYS:
-            monkeypatch.delenv(k, raising=False)
+        import paper_2511_21431_amd as m
+        m.memfine_set_launch_options()
         case = mw.make_case(w, seed)
         dev = device_case(w, case)
         _cache[key] = (dev, _run(w, dev, C))
@@ -60,26 +64,27 @@ def _reference(w, seed, C, monkeypatch):
 
 
 @pytest.mark.parametrize("C", [1, 3])
-@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda c: ",".join(f"{k[8:].lower()}={v}" for k, v in c.items()))
-def test_bitwise_across_launch_configs(mf, monkeypatch, cfg, C):
-    dev, ref = _reference(W_BIG, 61, C, monkeypatch)
-    for k in KEYS:
-        monkeypatch.delenv(k, raising=False)
-    for k, v in cfg.items():
-        monkeypatch.setenv(k, v)
+@pytest.mark.parametrize("cfg", CONFIGS, ids=_ids)
+def test_bitwise_across_launch_configs(mf, cfg, C):
+    dev, ref = _reference(W_BIG, 61, C)
     log(f"launch config {cfg} C={C}")
-    got = _run(W_BIG, dev, C)
+    try:
+        mf.memfine_set_launch_options(**cfg)
+        got = _run(W_BIG, dev, C)
+    finally:
+        mf.memfine_set_launch_options()
     for key in ref:
         assert np.array_equal(got[key], ref[key]), (cfg, C, key)
 
 
-@pytest.mark.parametrize("cfg", [{"MEMFINE_RASTER": "3"}, {"MEMFINE_SPLIT": "0"}, {"MEMFINE_STREAMS": "1"}],
-                         ids=lambda c: ",".join(f"{k[8:].lower()}={v}" for k, v in c.items()))
-def test_bitwise_across_launch_configs_f32(mf, monkeypatch, cfg):
-    dev, ref = _reference(W_F32, 5, 2, monkeypatch)
-    for k, v in cfg.items():
-        monkeypatch.setenv(k, v)
+@pytest.mark.parametrize("cfg", [{"raster": 3}, {"split_tail": False}, {"streams": True}], ids=_ids)
+def test_bitwise_across_launch_configs_f32(mf, cfg):
+    dev, ref = _reference(W_F32, 5, 2)
     log(f"launch config f32 {cfg}")
-    got = _run(W_F32, dev, 2)
+    try:
+        mf.memfine_set_launch_options(**cfg)
+        got = _run(W_F32, dev, 2)
+    finally:
+        mf.memfine_set_launch_options()
     for key in ref:
         assert np.array_equal(got[key], ref[key]), (cfg, key)

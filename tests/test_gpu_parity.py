@@ -210,17 +210,20 @@ def test_chunk_invariance_and_determinism(mf, name):
                 assert relerr(B[key], ref_B[key]) < 1e-5, (C, key)
 
 
-def test_side_stream_backward_bitwise(mf, monkeypatch):
+def test_side_stream_backward_bitwise(mf):
     """The optional side-stream schedule of the backward (weight gradients
     beside the FC1 dgrad) gives bit-identical results to the serial one."""
     w, case = small_case("cfg2-like")
     dev = device_case(w, case)
     for C in (1, 3):
         log(f"side streams C={C}")
-        monkeypatch.setenv("MEMFINE_STREAMS", "0")
+        mf.memfine_set_launch_options()
         ref = {k: host(v) for k, v in run_bwd(w, dev, C).items()}
-        monkeypatch.setenv("MEMFINE_STREAMS", "1")
-        got = {k: host(v) for k, v in run_bwd(w, dev, C).items()}
+        try:
+            mf.memfine_set_launch_options(streams=True)
+            got = {k: host(v) for k, v in run_bwd(w, dev, C).items()}
+        finally:
+            mf.memfine_set_launch_options()
         for key in ref:
             assert np.array_equal(got[key], ref[key]), (C, key)
 
@@ -253,6 +256,44 @@ def test_internal_workspace_per_stream(mf):
         for name in ("a", "b"):
             for key, v in got[name].items():
                 assert np.array_equal(host(v), ref[name][key]), (rep, name, key)
+
+
+def test_workspace_held_and_trim(mf):
+    """The cached workspace block of a stream (calls without an allocator)
+    grows to the largest chunk asked for, is reported by
+    memfine_workspace_held, and memfine_workspace_trim shrinks it to the
+    workspace of the chunk count in use: a C = 1 call, then a C = 4 call,
+    then a trim to the C = 4 workspace leaves exactly that block, and later
+    C = 4 calls run in it with bit-identical results (Section 4.1: the peak
+    is the largest chunk's)."""
+    t = torch()
+    w, case = small_case("cfg4-like")
+    dev = device_case(w, case)
+    s = shape_of(w)
+    ws1 = mf.memfine_workspace_bytes(s, 1, mf.PASS_BWD)
+    ws4 = mf.memfine_workspace_bytes(s, 4, mf.PASS_BWD)
+    st = t.cuda.Stream()
+    with t.cuda.stream(st):
+        log("workspace held / trim")
+        mf.memfine_workspace_trim(0)
+        assert mf.memfine_workspace_held() == 0
+        mf.memfine_pool_high_water(reset=True)
+        run_bwd(w, dev, 1)
+        assert mf.memfine_workspace_held() == ws1
+        first4 = {k: host(v) for k, v in run_bwd(w, dev, 4).items()}
+        assert mf.memfine_workspace_held() == ws1          # kept, not shrunk by itself
+        mf.memfine_workspace_trim(ws4)
+        assert mf.memfine_workspace_held() == ws4
+        again4 = {k: host(v) for k, v in run_bwd(w, dev, 4).items()}
+        assert mf.memfine_workspace_held() == ws4
+        for key in first4:
+            assert np.array_equal(first4[key], again4[key]), key
+        mf.memfine_workspace_trim(ws4 + 1)                  # larger than held: no change
+        assert mf.memfine_workspace_held() == ws4
+        mf.memfine_workspace_trim(0)
+        assert mf.memfine_workspace_held() == 0
+    st.synchronize()
+    assert mf.memfine_pool_high_water() >= ws1
 
 
 def test_accumulate_dW(mf):
@@ -394,7 +435,6 @@ def test_allocator_hook_peak_and_oom(mf):
 
 
 # ---------------------------------------------------- full-size, sampled
-# (5, 16): the budget sweep's largest chunk count on its 131072-token batch
 def test_full_size_workload2_every_output(mf):
     """The benchmark's workload (T=8192, h=2048, F=1408, E=16, top-4, the
     planner's C=2) checked in full against the oracle: every Y, dX and dgates
@@ -423,7 +463,11 @@ def test_full_size_workload2_every_output(mf):
         assert e <= TOL["bf16"], (key, e)
 
 
-FULL = [(2, 2), (2, 1), (3, 4), (4, 4), (5, 16)]
+# the benchmark's workload 2 at its planner C and C = 1; workloads 3 and 5 at
+# the chunk counts their planner picks at the benchmark budgets (C = 8 for
+# both), workload 3 at C = 4, workload 4 at its planner C, and the budget
+# sweep's largest chunk count on workload 5's 131072 tokens
+FULL = [(2, 2), (2, 1), (3, 4), (3, 8), (4, 4), (5, 8), (5, 16)]
 
 
 @pytest.mark.parametrize("cfg,C", FULL)
@@ -464,12 +508,14 @@ def test_full_size_sampled(mf, cfg, C):
     errs = {"Y": relerr(host(Y[toks]), Y_ref), "dX": relerr(host(B["dX"][toks]), dX_ref),
             "dgates": relerr(host(B["dgates"][toks]), dg_ref)}
     fs = sorted(set(rng.choice(w.F, size=3, replace=False).tolist()) | {0, w.F - 1})
+    # the hottest, the median and the coldest expert; the oracle's column
+    # form sums over blocks of 32768 slots, so the hot expert of workload 5
+    # (524288 slots: weight-gradient tiles with K up to 524288 rows) is
+    # checked too
     dw_experts = [int(order[0]), int(order[w.E // 2]), int(order[-1])]
-    if counts[dw_experts[0]] > 20000:
-        # the oracle's column form re-runs the expert's whole forward in fp64:
-        # a 500k-row hot expert is minutes of CPU, so check the others
-        dw_experts = dw_experts[1:]
     for e in dw_experts:
+        log(f"full-size cfg{cfg} C={C}: weight-gradient columns of expert {e} "
+            f"({int(counts[e])} slots)")
         g1, u1, c2 = om.moe_dW_expert_columns(X, idx, gates, W1l, W2l, dY, e, fs)
         errs[f"dW1g[{e}]"] = relerr(host(B["dW1"][e][fs]), g1)
         errs[f"dW1u[{e}]"] = relerr(host(B["dW1"][e][[w.F + f for f in fs]]), u1)

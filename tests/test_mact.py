@@ -200,3 +200,12 @@ def test_replay_skew_schedule(mf):
     early, late = C[5:16, :8], C[5:16, 8:]
     assert late.mean() > early.mean() and C.max() > 1
     assert (C[25:] == 1).all() and (C[:2] == 1).all()
+
+
+@pytest.mark.gpu
+def test_mact_model_I_in_the_gpu_suite(mf):
+    """The library's MACT entry points for Model I at every pipeline rank,
+    with and without full recomputation, against the oracle (the same check
+    smoke() runs on the GPU machine)."""
+    import __graft_entry__ as entry
+    entry._smoke_mact(mf)

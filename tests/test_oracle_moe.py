@@ -245,7 +245,10 @@ def test_dW_columns_match_full():
     B = om.moe_bwd(X, idx, g, W1, W2, dY, 2)
     fs = [0, 3, 7]
     for e in range(4):
-        g1, u1, c2 = om.moe_dW_expert_columns(X, idx, g, W1, W2, dY, e, fs)
-        assert rel(g1, B["dW1"][e][fs]) < 1e-12
-        assert rel(u1, B["dW1"][e][[8 + f for f in fs]]) < 1e-12
-        assert rel(c2, B["dW2"][e][:, fs]) < 1e-12
+        # whole, and summed over blocks of 1, 2 and 5 slots (the form used for
+        # experts with half a million slots)
+        for block in (32768, 1, 2, 5):
+            g1, u1, c2 = om.moe_dW_expert_columns(X, idx, g, W1, W2, dY, e, fs, block=block)
+            assert rel(g1, B["dW1"][e][fs]) < 1e-12
+            assert rel(u1, B["dW1"][e][[8 + f for f in fs]]) < 1e-12
+            assert rel(c2, B["dW2"][e][:, fs]) < 1e-12
