@@ -51,6 +51,9 @@ DEFAULT_BUDGET = {1: 64 * 1024, 2: 250 * 10**6, 3: 500 * 10**6, 4: 10**9, 5: 8 *
 # each budget's C is joined with the measured chunk sweep
 BUDGET_SWEEP = {5: [4 * 10**9, 8 * 10**9, 16 * 10**9, 32 * 10**9, 64 * 10**9],
                 3: [5 * 10**8, 10**9, 13 * 10**8, 2 * 10**9, 25 * 10**8, 4 * 10**9]}
+# router logits per token: the 32 local experts of workloads 4 and 5 are one
+# GPU's slice of a 256-expert model (the paper's Table 3 models)
+ROUTER_WIDTH = {4: 256, 5: 256}
 GEMMS = ("fc1", "fc2", "fc1_recompute", "fc2_dgrad", "fc2_wgrad", "fc1_wgrad", "fc1_dgrad")
 GEMM_TARGET = 0.60   # share of the bf16 MFMA peak the grouped GEMMs aim for
 
@@ -437,8 +440,8 @@ def main():
 
     # ---- the router in front of the layer: its kernels, and the whole block
     router = None
-    if not args.no_router and w.E <= 64 and w.k <= 16:
-        router = bench_router(mf, torch, w, shape, dev, step, args.steps)
+    if not args.no_router and w.k <= 16:
+        router = bench_router(mf, torch, w, dev, step, args.steps, ROUTER_WIDTH.get(cfg, w.E))
 
     # ---- the oracle on the host cores, bounded sample of the same workload
     cpu = None
@@ -595,18 +598,20 @@ def layer_bound_ms(prof, peak_tflops):
                for v in prof.values())
 
 
-def bench_router(mf, torch, w, shape, dev, layer_step, steps):
-    """Router forward and backward at the workload's shapes (HBM-bound:
-    achieved algorithmic GB/s against 8 TB/s), and the trainable block router
-    -> chunked layer -> layer backward -> router backward in tokens/s."""
+def bench_router(mf, torch, w, dev, layer_step, steps, E_r):
+    """Router forward and backward at the workload's shapes with E_r logits
+    per token (HBM-bound: achieved algorithmic GB/s against 8 TB/s), and the
+    trainable block router -> chunked layer -> layer backward -> router
+    backward in tokens/s."""
     dt = dev["X"].dtype
+    shape = mf.make_shape(w.T, w.h, w.F, E_r, w.k, mf.BF16 if w.dtype == "bf16" else mf.F32)
     gen = torch.Generator(device="cuda").manual_seed(4242)
-    Wr = (torch.randn((w.E, w.h), generator=gen, device="cuda") / w.h ** 0.5).to(dt)
+    Wr = (torch.randn((E_r, w.h), generator=gen, device="cuda") / w.h ** 0.5).to(dt)
     idx = torch.empty((w.T, w.k), dtype=torch.int32, device="cuda")
     gates = torch.empty((w.T, w.k), device="cuda")
     dgr = torch.randn((w.T, w.k), generator=gen, device="cuda")
     dXr = torch.zeros((w.T, w.h), dtype=dt, device="cuda")
-    dWr = torch.empty((w.E, w.h), device="cuda")
+    dWr = torch.empty((E_r, w.h), device="cuda")
 
     def fwd_bwd():
         mf.memfine_router_fwd(shape, dev["X"], Wr, idx, gates)
@@ -648,7 +653,7 @@ def bench_router(mf, torch, w, shape, dev, layer_step, steps):
     log(f"[bench] router: " + ", ".join(f"{k} {v['avg_ms']:.4f} ms {v['gbs']:.0f} GB/s"
                                          for k, v in kern.items())
         + f"; block {w.T / block_s:.0f} tokens/s")
-    return {"kernels": kern, "block_tokens_per_s": round(w.T / block_s, 1),
+    return {"router_experts": E_r, "kernels": kern, "block_tokens_per_s": round(w.T / block_s, 1),
             "block_ms_per_step": round(block_s * 1e3, 4),
             "note": "router fwd + chunked layer fwd/bwd (same plan as the headline step) + "
                     "router bwd accumulating into dX; the layer's routing stays the "

@@ -321,7 +321,8 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
  * Router in front of the expert layer (Table 2 rows 9-10 store its input and
  * its logits; the gates it produces are the scores that multiply the expert
  * outputs, Table 2 "score mul").  `shape` is the layer's shape; the router
- * needs k <= 16 and k <= E <= 64 (MEMFINE_ERR_UNSUPPORTED otherwise).
+ * needs k <= 16 and k <= E <= 256 (MEMFINE_ERR_UNSUPPORTED otherwise): up to
+ * the 256 routed experts of the paper's Table 3 models.
  *
  * Forward: logits = X Wr^T (fp32 accumulation), softmax over the E experts,
  * the k largest logits (equal logits: the lower expert id first), and the

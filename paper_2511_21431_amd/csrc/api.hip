@@ -816,7 +816,7 @@ int router_ep(int E) { return (E + 31) / 32 * 32; }
 int check_router(const memfine_shape* shape) {
   int rc = check_shape(shape);
   if (rc) return rc;
-  if (shape->k > 16 || shape->k > shape->E || shape->E > 64) return MEMFINE_ERR_UNSUPPORTED;
+  if (shape->k > 16 || shape->k > shape->E || shape->E > 256) return MEMFINE_ERR_UNSUPPORTED;
   return MEMFINE_OK;
 }
 }  // namespace

@@ -81,7 +81,7 @@ struct GemmArgs {
 
 int dgate_partials(int F);
 
-// Router (E <= 64 experts, k <= 16): logits on the matrix cores, softmax,
+// Router (E <= 256 experts, k <= 16): logits on the matrix cores, softmax,
 // top-k and renormalised gates; logits may be null.
 hipError_t launch_router_fwd(int dtype, const void* X, const void* Wr, int64_t T, int h, int E,
                              int k, int32_t* idx, float* gates, float* logits, hipStream_t s);

@@ -180,6 +180,128 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_fwd_kernel(
   }
 }
 
+// Forward for wide routers (64 < E <= 256 logits per token, the width of a
+// 256-expert model).  A workgroup owns 32 tokens; wave w multiplies them
+// with expert blocks w NBW .. w NBW + NBW - 1 (32 experts each) over the
+// whole K, operands loaded straight into registers one K block ahead.  The
+// logits go to LDS; then each wave selects the top-k of 8 of the tokens,
+// one token at a time: lane l holds experts l, l + 64, l + 128, l + 192,
+// and each of the k rounds is a wave-wide arg-max over (logit, lower id)
+// by shuffles, so the selection and its order are those of the narrow
+// kernel.
+template <typename T, int NBW>
+__global__ __launch_bounds__(64 * kRouterWaves) void router_fwd_wide_kernel(
+    const T* __restrict__ X, const T* __restrict__ Wr, int64_t T_, int h, int E, int k,
+    int32_t* __restrict__ idx, float* __restrict__ gates, float* __restrict__ logits) {
+  typedef RK<T> K;
+  constexpr int kMaxE = 32 * NBW * kRouterWaves;
+  __shared__ float lg[32][kMaxE + 1];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r = lane & 31, hh = lane >> 5;
+  const int64_t t0 = (int64_t)blockIdx.x * 32;
+  const int64_t trow = min(t0 + r, T_ - 1);  // rows past T read the last row
+  const T* xr = X + trow * h;
+  const T* wr[NBW];
+#pragma unroll
+  for (int nb = 0; nb < NBW; ++nb)
+    wr[nb] = Wr + (int64_t)min(32 * (w * NBW + nb) + r, E - 1) * h;
+  f32x16_t acc[NBW];
+#pragma unroll
+  for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) acc[nb][q] = 0.f;
+  const bool any = 32 * w * NBW < E;  // a wave past the last expert block skips the product
+  typename K::Raw a[2], b[2][NBW];
+  const int nkb = h / K::KB;
+  if (any) {
+    K::load(xr, 0, hh, a[0]);
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) K::load(wr[nb], 0, hh, b[0][nb]);
+    for (int kb = 0; kb < nkb; kb += 2) {
+      if (kb + 1 < nkb) {
+        K::load(xr, kb + 1, hh, a[1]);
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) K::load(wr[nb], kb + 1, hh, b[1][nb]);
+      }
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb) K::mma(a[0], b[0][nb], acc[nb]);
+      if (kb + 1 >= nkb) break;
+      if (kb + 2 < nkb) {
+        K::load(xr, kb + 2, hh, a[0]);
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) K::load(wr[nb], kb + 2, hh, b[0][nb]);
+      }
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb) K::mma(a[1], b[1][nb], acc[nb]);
+    }
+  }
+  // lane l holds, for token l % 32, experts 32 blk + 8 (q / 4) + 4 (l / 32) + q % 4
+#pragma unroll
+  for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+    for (int q = 0; q < 16; ++q)
+      lg[r][32 * (w * NBW + nb) + 8 * (q >> 2) + 4 * hh + (q & 3)] = acc[nb][q];
+  __syncthreads();
+  constexpr int V = kMaxE / 64;  // logits per lane per token
+  for (int tt = 0; tt < 32 / kRouterWaves; ++tt) {
+    const int tok = w * (32 / kRouterWaves) + tt;
+    const int64_t t = t0 + tok;
+    if (t >= T_) break;  // uniform over the wave
+    float v[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const int e = lane + 64 * j;
+      v[j] = lg[tok][e];
+      if (logits && e < E) logits[t * E + e] = v[j];
+    }
+    uint32_t taken = 0;
+    float selv[16];
+    int seli[16];
+    for (int j = 0; j < k; ++j) {
+      float bv = -INFINITY;
+      int bi = INT32_MAX;
+#pragma unroll
+      for (int q = 0; q < V; ++q) {
+        const int e = lane + 64 * q;
+        if (e < E && !((taken >> q) & 1u) && (v[q] > bv || (v[q] == bv && e < bi))) {
+          bv = v[q];
+          bi = e;
+        }
+      }
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) {
+        const float ov = __shfl_xor(bv, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (ov > bv || (ov == bv && oi < bi)) {
+          bv = ov;
+          bi = oi;
+        }
+      }
+      if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
+#pragma unroll
+      for (int jj = 0; jj < 16; ++jj)
+        if (jj == j) {
+          selv[jj] = bv;
+          seli[jj] = bi;
+        }
+    }
+    // renormalised softmax over the selected logits; selv[0] is the largest
+    float e[16], sum = 0.f;
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj) {
+      e[jj] = jj < k ? __expf(selv[jj] - selv[0]) : 0.f;
+      sum += e[jj];
+    }
+    const float inv = 1.f / sum;
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj)
+      if (jj < k && lane == jj) {
+        idx[t * k + jj] = seli[jj];
+        gates[t * k + jj] = e[jj] * inv;
+      }
+  }
+}
+
 // Backward, one wave per token (grid-stride): dz_j = g_j (dg_j - sum g dg);
 // dX[t] (+)= sum_j dz_j Wr[i_j]; the dense row D[t, 0..EP) = dz scattered to
 // the selected experts (bf16 or fp32, zero elsewhere) for the weight-gradient
@@ -311,15 +433,25 @@ hipError_t launch_router_fwd(int dtype, const void* X, const void* Wr, int64_t T
   const int blocks = (int)((T + 31) / 32);
   const dim3 grid(blocks), block(64 * kRouterWaves);
   if (dtype == 0) {
+    const bf16_t *x = (const bf16_t*)X, *wr = (const bf16_t*)Wr;
     if (E <= 32)
-      router_fwd_kernel<bf16_t, 1><<<grid, block, 0, s>>>((const bf16_t*)X, (const bf16_t*)Wr, T, h, E, k, idx, gates, logits);
+      router_fwd_kernel<bf16_t, 1><<<grid, block, 0, s>>>(x, wr, T, h, E, k, idx, gates, logits);
+    else if (E <= 64)
+      router_fwd_kernel<bf16_t, 2><<<grid, block, 0, s>>>(x, wr, T, h, E, k, idx, gates, logits);
+    else if (E <= 128)
+      router_fwd_wide_kernel<bf16_t, 1><<<grid, block, 0, s>>>(x, wr, T, h, E, k, idx, gates, logits);
     else
-      router_fwd_kernel<bf16_t, 2><<<grid, block, 0, s>>>((const bf16_t*)X, (const bf16_t*)Wr, T, h, E, k, idx, gates, logits);
+      router_fwd_wide_kernel<bf16_t, 2><<<grid, block, 0, s>>>(x, wr, T, h, E, k, idx, gates, logits);
   } else {
+    const float *x = (const float*)X, *wr = (const float*)Wr;
     if (E <= 32)
-      router_fwd_kernel<float, 1><<<grid, block, 0, s>>>((const float*)X, (const float*)Wr, T, h, E, k, idx, gates, logits);
+      router_fwd_kernel<float, 1><<<grid, block, 0, s>>>(x, wr, T, h, E, k, idx, gates, logits);
+    else if (E <= 64)
+      router_fwd_kernel<float, 2><<<grid, block, 0, s>>>(x, wr, T, h, E, k, idx, gates, logits);
+    else if (E <= 128)
+      router_fwd_wide_kernel<float, 1><<<grid, block, 0, s>>>(x, wr, T, h, E, k, idx, gates, logits);
     else
-      router_fwd_kernel<float, 2><<<grid, block, 0, s>>>((const float*)X, (const float*)Wr, T, h, E, k, idx, gates, logits);
+      router_fwd_wide_kernel<float, 2><<<grid, block, 0, s>>>(x, wr, T, h, E, k, idx, gates, logits);
   }
   return hipGetLastError();
 }

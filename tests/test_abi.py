@@ -235,7 +235,7 @@ def test_router_limits_and_null_pointers_rejected_on_host():
     L = _lib.lib()
     fake = ctypes.c_void_p(0x1000)
     ok = mf.make_shape(16, 64, 64, 8, 2, mf.BF16)
-    for bad in (mf.make_shape(16, 64, 64, 65, 2, mf.BF16),    # E > 64
+    for bad in (mf.make_shape(16, 64, 64, 257, 2, mf.BF16),   # E > 256
                 mf.make_shape(16, 64, 64, 32, 17, mf.BF16),   # k > 16
                 mf.make_shape(16, 64, 64, 3, 4, mf.BF16)):    # k > E
         assert L.memfine_router_fwd(ctypes.byref(bad), fake, fake, fake, fake, None, None) == -2
