@@ -65,6 +65,7 @@ extern "C" {
 #define MEMFINE_ERR_BUDGET       (-3)
 #define MEMFINE_ERR_OOM          (-4)
 #define MEMFINE_ERR_HIP          (-5)
+#define MEMFINE_ERR_SCRATCH      (-6)
 
 /* element types */
 #define MEMFINE_BF16  0
@@ -304,6 +305,28 @@ int memfine_mact_select(const int32_t* bins, const int64_t* thresholds, int32_t 
 int memfine_moe_fwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
                     const int32_t* d_idx, const float* d_gates, const void* d_W1,
                     const void* d_W2, void* d_Y, const memfine_allocator* alloc, void* stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * chunked forward of memfine_moe_fwd, same arguments (no allocator) and
+ * bit-identical results, with every chunk's working buffers in one static
+ * device array of MEMFINE_NOALLOC_SCRATCH_BYTES (64 MiB) that the library's
+ * code object carries; each GPU the library runs on holds its own copy until
+ * the process ends.  The call allocates and frees nothing (no hipMalloc,
+ * pool or allocator call; the array's address is looked up once per device
+ * with hipGetSymbolAddress).  A call whose largest chunk needs more than the
+ * array, memfine_workspace_bytes(shape, chunks, MEMFINE_PASS_FWD) >
+ * MEMFINE_NOALLOC_SCRATCH_BYTES, returns MEMFINE_ERR_SCRATCH before anything
+ * is enqueued: raise `chunks`.  Nothing in the array needs to start at zero
+ * (every buffer is written before it is read).  All calls on one GPU share
+ * its array: calls that overlap on one GPU (other streams, other threads)
+ * race, and the caller must order them (e.g. one stream).
+ */
+#define MEMFINE_NOALLOC_SCRATCH_BYTES (64ll << 20)
+int memfine_moe_fwd_noalloc(const memfine_shape* shape, int32_t chunks, const void* d_X,
+                            const int32_t* d_idx, const float* d_gates, const void* d_W1,
+                            const void* d_W2, void* d_Y, void* stream);
 
 /*
  * Chunked-recompute backward, Eq. (7): for each chunk in ascending order,

@@ -17,6 +17,8 @@ import numpy as np
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmemfine.so")
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_BUDGET, ERR_OOM, ERR_HIP = 0, -1, -2, -3, -4, -5
+ERR_SCRATCH = -6
+NOALLOC_SCRATCH_BYTES = 64 << 20
 BF16, F32 = 0, 1
 PASS_FWD, PASS_BWD = 0, 1
 
@@ -98,6 +100,7 @@ _SIGS = {
     "memfine_set_launch_options": (ctypes.c_int, [ctypes.POINTER(LaunchOptions)]),
     "memfine_get_launch_options": (ctypes.c_int, [ctypes.POINTER(LaunchOptions)]),
     "memfine_moe_fwd": (ctypes.c_int, [SHP, ctypes.c_int32, P, P, P, P, P, P, ALP, P]),
+    "memfine_moe_fwd_noalloc": (ctypes.c_int, [SHP, ctypes.c_int32, P, P, P, P, P, P, P]),
     "memfine_moe_bwd": (ctypes.c_int, [SHP, ctypes.c_int32, P, P, P, P, P, P, P, P, P, P,
                                        ctypes.c_int32, ALP, P]),
     "memfine_static_memory": (ctypes.c_int, [I64P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -385,6 +388,22 @@ def memfine_moe_fwd(shape: Shape, chunks: int, X, idx, gates, W1, W2, Y, allocat
         _ptr(W1, (E, 2 * F, h), dt, "W1"), _ptr(W2, (E, h, F), dt, "W2"),
         _ptr(Y, (T, h), dt, "Y"), _alloc_arg(allocator), _stream(stream))
     _check(rc, "memfine_moe_fwd")
+
+
+def memfine_moe_fwd_noalloc(shape: Shape, chunks: int, X, idx, gates, W1, W2, Y,
+                            stream=None) -> None:
+    """memfine_moe_fwd with the chunk buffers in the library's static device
+    scratch (no allocation); MemfineError(ERR_SCRATCH) when the largest chunk
+    needs more than NOALLOC_SCRATCH_BYTES."""
+    torch = _torch()
+    dt = _dt(shape)
+    T, h, F, E, k = shape.T, shape.h, shape.F, shape.E, shape.k
+    rc = lib().memfine_moe_fwd_noalloc(
+        ctypes.byref(shape), int(chunks), _ptr(X, (T, h), dt, "X"),
+        _ptr(idx, (T, k), torch.int32, "idx"), _ptr(gates, (T, k), torch.float32, "gates"),
+        _ptr(W1, (E, 2 * F, h), dt, "W1"), _ptr(W2, (E, h, F), dt, "W2"),
+        _ptr(Y, (T, h), dt, "Y"), _stream(stream))
+    _check(rc, "memfine_moe_fwd_noalloc")
 
 
 def memfine_moe_bwd(shape: Shape, chunks: int, X, idx, gates, W1, W2, dY, dX, dW1, dW2, dgates,

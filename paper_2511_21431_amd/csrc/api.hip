@@ -377,6 +377,41 @@ struct Work {
 };
 Work dispatch_work(int64_t n) { return {0.0, 8.0 * n + 16.0 * n}; }
 
+// ----------------------------------------------- static scratch (no-alloc)
+// Working memory of memfine_moe_fwd_noalloc: a device array that the code
+// object carries, so that the call allocates nothing.  In host code its name
+// stands for a host-side shadow, not a device address: the address comes
+// from hipGetSymbolAddress, once per device (each GPU holds its own copy),
+// and is the only way host code refers to the array's memory.
+constexpr int64_t kScratchBytes = MEMFINE_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+std::unordered_map<int, void*> g_scratch_ptr;
+
+// Device address of `scratch` on the current device (looked up on the first
+// call on that device, with it current).
+int scratch_address(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MEMFINE_ERR_HIP;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  auto it = g_scratch_ptr.find(dev);
+  if (it == g_scratch_ptr.end()) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+      (void)hipGetLastError();
+      return MEMFINE_ERR_HIP;
+    }
+    it = g_scratch_ptr.emplace(dev, ptr).first;
+  }
+  *out = it->second;
+  return MEMFINE_OK;
+}
+
+int moe_fwd_impl(const memfine_shape* shape, int32_t chunks, const void* d_X,
+                 const int32_t* d_idx, const float* d_gates, const void* d_W1, const void* d_W2,
+                 void* d_Y, const memfine_allocator* alloc, void* fixed_ws, void* stream);
+
 }  // namespace
 
 // =================================================================== ABI
@@ -390,6 +425,9 @@ const char* memfine_status_str(int status) {
     case MEMFINE_ERR_BUDGET: return "memory budget too small for every allowed chunk count";
     case MEMFINE_ERR_OOM: return "device memory allocation failed";
     case MEMFINE_ERR_HIP: return "HIP runtime error";
+    case MEMFINE_ERR_SCRATCH:
+      return "the largest chunk needs more working memory than the static scratch holds "
+             "(MEMFINE_NOALLOC_SCRATCH_BYTES); use more chunks";
     default: return "unknown status";
   }
 }
@@ -610,6 +648,34 @@ int memfine_dispatch(const memfine_shape* shape, const int32_t* d_idx, int64_t t
 int memfine_moe_fwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
                     const int32_t* d_idx, const float* d_gates, const void* d_W1,
                     const void* d_W2, void* d_Y, const memfine_allocator* alloc, void* stream) {
+  return moe_fwd_impl(shape, chunks, d_X, d_idx, d_gates, d_W1, d_W2, d_Y, alloc, nullptr, stream);
+}
+
+int memfine_moe_fwd_noalloc(const memfine_shape* shape, int32_t chunks, const void* d_X,
+                            const int32_t* d_idx, const float* d_gates, const void* d_W1,
+                            const void* d_W2, void* d_Y, void* stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if (chunks < 1) return MEMFINE_ERR_INVALID_ARG;
+  if (memfine_workspace_bytes(shape, chunks, MEMFINE_PASS_FWD) > kScratchBytes)
+    return MEMFINE_ERR_SCRATCH;
+  if (shape->T == 0) return MEMFINE_OK;
+  void* scratch_dev = nullptr;
+  rc = scratch_address(&scratch_dev);
+  if (rc) return rc;
+  return moe_fwd_impl(shape, chunks, d_X, d_idx, d_gates, d_W1, d_W2, d_Y, nullptr, scratch_dev,
+                      stream);
+}
+
+}  // extern "C"
+
+namespace {
+// The chunked forward.  Each chunk's buffers come from `fixed_ws` when it is
+// not null (it then holds the largest chunk's workspace; nothing is
+// allocated or released), else from ws_alloc / ws_release.
+int moe_fwd_impl(const memfine_shape* shape, int32_t chunks, const void* d_X,
+                 const int32_t* d_idx, const float* d_gates, const void* d_W1, const void* d_W2,
+                 void* d_Y, const memfine_allocator* alloc, void* fixed_ws, void* stream) {
   int rc = check_shape(shape);
   if (rc) return rc;
   if (chunks < 1) return MEMFINE_ERR_INVALID_ARG;
@@ -626,7 +692,7 @@ int memfine_moe_fwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
     if (n == 0) continue;
     Layout L;
     chunk_layout(S, n, MEMFINE_PASS_FWD, L);
-    void* ws = ws_alloc(alloc, (size_t)L.total, s);
+    void* ws = fixed_ws ? fixed_ws : ws_alloc(alloc, (size_t)L.total, s);
     if (!ws) return MEMFINE_ERR_OOM;
     const ChunkBuffers cb = carve(ws, L);
     GemmArgs g = gemm_args(S, n, cb, opt);
@@ -654,11 +720,14 @@ int memfine_moe_fwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
       err = launch_combine(S.dtype, cb.y, cb.m.row_of_slot, d_gates, t0, (int)tokens, S.h, S.k,
                            d_Y, s);
     }
-    ws_release(alloc, ws, (size_t)L.total, s);
+    if (!fixed_ws) ws_release(alloc, ws, (size_t)L.total, s);
     if (err != hipSuccess) return MEMFINE_ERR_HIP;
   }
   return MEMFINE_OK;
 }
+}  // namespace
+
+extern "C" {
 
 int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
                     const int32_t* d_idx, const float* d_gates, const void* d_W1,
