@@ -153,12 +153,14 @@ def summarize_traffic(d, cfg, path=None):
                 e[key + "_bytes"] += float(r["Counter_Value"]) * 1024.0 * scale[key]
     if not per:
         raise SystemExit("no FC1 weight-gradient dispatches in the counter files")
+    # mean over every profiled launch: the two dW modes (the first chunk
+    # writes dW, the others accumulate) weighted as a step runs them
+    n_all = sum(e["launches"] for e in per.values())
+    fetch = sum(e["fetch_bytes"] for e in per.values()) / n_all
+    write = sum(e["write_bytes"] for e in per.values()) / n_all
     for e in per.values():
         e["fetch_bytes"] /= e["launches"]
         e["write_bytes"] /= e["launches"]
-    # mean over the two dW modes, one launch of each per step
-    fetch = sum(e["fetch_bytes"] for e in per.values()) / len(per)
-    write = sum(e["write_bytes"] for e in per.values()) / len(per)
     out = {"kernel": "fc1_wgrad", "rocprof_name": " + ".join(sorted(per)),
            "launches_profiled": sum(e["launches"] for e in per.values()), "per_kernel": per,
            "fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,

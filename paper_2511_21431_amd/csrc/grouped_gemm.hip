@@ -53,7 +53,7 @@
 namespace memfine {
 namespace {
 
-constexpr int kThreads = 256;
+
 constexpr uint32_t kOOB = 0x80000000u;    // byte offset past every buffer's range
 #ifndef MEMFINE_SCHED_HINTS
 #define MEMFINE_SCHED_HINTS 1
