@@ -46,12 +46,16 @@ def test_traffic_summary(tmp_path):
     write_csv(tmp_path / "WRITE_SIZE_counter_collection.csv", write)
     out = tmp_path / "traffic.json"
     d = bench.summarize_traffic(str(tmp_path), 2, path=str(out))
-    # per kernel means (KiB x 1024 x scale), then the mean of the two dW modes
+    # per kernel means (KiB x 1024 x scale); the per-launch figure is the
+    # mean over all profiled launches (the dW modes as often as a step runs
+    # them: here two launches that write dW and one that accumulates)
     f0, f1 = 2000.0 * 1024 * 2, 5000.0 * 1024 * 2
     w0, w1 = 200.0 * 1024, 700.0 * 1024
-    assert d["fetch_bytes_per_launch"] == pytest.approx((f0 + f1) / 2)
-    assert d["write_bytes_per_launch"] == pytest.approx((w0 + w1) / 2)
-    assert d["bytes_per_launch"] == pytest.approx((f0 + f1 + w0 + w1) / 2)
+    assert d["fetch_bytes_per_launch"] == pytest.approx((2 * f0 + f1) / 3)
+    assert d["write_bytes_per_launch"] == pytest.approx((2 * w0 + w1) / 3)
+    assert d["bytes_per_launch"] == pytest.approx((2 * (f0 + w0) + f1 + w1) / 3)
+    per = sorted(d["per_kernel"].values(), key=lambda e: e["launches"])
+    assert per[0]["fetch_bytes"] == pytest.approx(f1) and per[1]["fetch_bytes"] == pytest.approx(f0)
     assert d["launches_profiled"] == 3
     assert d["source_sha256_16"] == bench.source_digest("grouped_gemm.hip")
     assert json.loads(out.read_text())["bytes_per_launch"] == pytest.approx(d["bytes_per_launch"])
