@@ -1449,7 +1449,11 @@ template <typename T, class C, class P, int kArray = 0, class Next = NoNext>
 __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p, const Tile& t,
                                             bool prefetched = false, Next next = Next(),
                                             bool deep = false) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  // the wave index in a scalar register: every LDS destination of a copy
+  // (M0) and every per-wave choice below is then scalar arithmetic, with no
+  // VGPR address and readfirstlane per copy instruction
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   int wm, wn;
   C::wave_role(w, wm, wn);
   // a wave whose whole block lies past the tile's rows or columns skips its
@@ -1653,7 +1657,7 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
         // the epilogue's own loads would wait behind earlier copies: issue
         // the next tile's copies once the epilogue is done
         run_located<T, C, P>(g, smem, p, t, pre);
-        next(smem, threadIdx.x >> 6, threadIdx.x & 63);
+        next(smem, __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), threadIdx.x & 63);
       }
       p = pn;
       t = tn;
