@@ -127,6 +127,15 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with "
                               "`python -m paper_2511_21431_amd.build` (there is no fallback)")
+        # torch first, when it is installed: the library then binds to the HIP
+        # runtime torch has loaded.  Loaded before torch, it would bring in the
+        # system's runtime, and torch would load its own beside it; two runtimes
+        # in one process share neither device memory nor streams, and the
+        # library's first launch on torch's tensors fails.
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         L = ctypes.CDLL(LIB_PATH)
         for name, (res, args) in _SIGS.items():
             fn = getattr(L, name)

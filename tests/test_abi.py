@@ -31,6 +31,20 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(_lib._SIGS), "binding and header disagree"
 
 
+def test_binding_shares_torch_hip_runtime():
+    """Whatever the import order, the process maps one HIP runtime: the
+    binding loads torch before the library (a library loaded first would bring
+    in a second runtime, and its launches on torch's tensors fail)."""
+    import subprocess
+    import sys
+    code = ("import paper_2511_21431_amd._lib as L; L.memfine_set_launch_options(); import torch; "
+            "print(len({l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}))")
+    out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
+                         timeout=600)
+    assert out.returncode == 0, out.stderr[-2000:]
+    assert out.stdout.strip().splitlines()[-1] == "1"
+
+
 def test_launch_options_roundtrip_and_validation():
     L = _lib.lib()
     mf.memfine_set_launch_options()
