@@ -194,6 +194,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
   const int32_t n = (int32_t)(bytes < (int64_t)kOOB ? bytes : (int64_t)kOOB - 1);
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
 }
+// a range the caller knows to be below 2^31 bytes (no clamp)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc32(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int32_t)bytes,
+                                           0x00020000);
+}
 
 __device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t voff,
                                            uint32_t soff) {
@@ -1158,6 +1163,12 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
   static constexpr int D = C::S - 1;              // token prefetch distance (K tiles)
   uint32_t colb[IG];         // gathered operand: byte of this lane's column in a row
   int32_t tok[D][IG];        // gathered operand: tokens of the next D K tiles' rows
+  // Per tile, uniform (scalar registers): the expert's row -> token entries,
+  // the first of its rows in the non-gathered operand, and its row count.
+  // Built once in init, so that a K step's copy issue is a few scalar adds.
+  __amdgpu_buffer_rsrc_t trs;
+  const char* pbase;
+  int Ku;
   __host__ __device__ static int M(const GemmArgs& g) { return kFC1 ? 2 * g.F : g.h; }
   __host__ __device__ static int N(const GemmArgs& g) { return kFC1 ? g.h : g.F; }
   __device__ __forceinline__ static bool acc_on(const GemmArgs& g) {
@@ -1224,28 +1235,33 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
   // for every copy in flight); rows past K read as 0 and are masked when the
   // copies are issued.  The values are not touched here, for the same
   // reason.
-  __device__ __forceinline__ void load_tokens(const GemmArgs& g, const Tile& t, int kt, int wave,
-                                              int lane, int32_t (&dst)[IG]) {
-    const int r0 = __builtin_amdgcn_readfirstlane(t.r0);
-    const int K = __builtin_amdgcn_readfirstlane(t.K);
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(g.tok_of_row + r0, (int64_t)max(K, 0) * 4);
+  __device__ __forceinline__ void load_tokens(int kt, int wave, int lane, int32_t (&dst)[IG]) {
 #pragma clang loop unroll(full)
     for (int i = 0; i < IG; ++i)
       dst[i] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(
-          rs, (uint32_t)k_row(0, i, wave, lane) * 4, (uint32_t)kt * OA::BKE * 4, 0);
+          trs, (uint32_t)k_row(0, i, wave, lane) * 4, (uint32_t)kt * OA::BKE * 4, 0);
   }
-  // the non-gathered operand (rows r0 .. r0+K of u for FC1, of ag for FC2) is
-  // re-based at every K tile, so its offsets stay small for any row count
+  // The non-gathered operand (rows r0 .. r0+K of u for FC1, of ag for FC2)
+  // gets a resource per K tile, based at the tile's first row, so offsets
+  // stay small for any row count and the range ends at the expert's last
+  // row (the rows of a last partial K tile past it read as 0).  The range
+  // is below 2^31 bytes: 64 rows of at most 2^25 bytes (the shape check
+  // bounds one expert's weight, 2 F h elements, below 2^31 bytes, h >= 64).
   __device__ __forceinline__ int ldp(const GemmArgs& g) const { return kFC1 ? 2 * g.F : g.F; }
-  __device__ __forceinline__ __amdgpu_buffer_rsrc_t plain_rsrc(const GemmArgs& g, const Tile& t,
-                                                               int kt) const {
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t plain_rsrc(const GemmArgs& g, int kt) const {
+    const uint32_t ldpb = (uint32_t)ldp(g) * sizeof(T);
     const int k0 = kt * OA::BKE;
-    const int rows = min(OA::BKE, t.K - k0);
-    return make_rsrc(cptr<T>(kFC1 ? g.u : g.ag, (int64_t)(t.r0 + k0) * ldp(g)),
-                     (int64_t)rows * ldp(g) * sizeof(T));
+    const int rows = min(OA::BKE, Ku - k0);
+    return make_rsrc32(pbase + (int64_t)k0 * ldpb, (uint32_t)rows * ldpb);
   }
   __device__ __forceinline__ void init(const GemmArgs& g, const Tile& t, int wave, int lane) {
     const uint32_t ldpb = (uint32_t)ldp(g) * sizeof(T);
+    // the tile is the workgroup's: its fields are uniform, which the compiler
+    // cannot always prove (the resources must sit in scalar registers)
+    const int r0 = __builtin_amdgcn_readfirstlane(t.r0);
+    Ku = __builtin_amdgcn_readfirstlane(t.K);
+    trs = make_rsrc(g.tok_of_row + r0, (int64_t)max(Ku, 0) * 4);
+    pbase = cptr<T>(kFC1 ? g.u : g.ag, (int64_t)r0 * ldp(g));
     const int pcol0 = kFC1 ? t.m0 : t.n0;
     const int plim = kFC1 ? M(g) : N(g);
     const __amdgpu_buffer_rsrc_t grs = make_rsrc(kFC1 ? g.X : g.dY, g.T_h_bytes);
@@ -1277,7 +1293,7 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
       }
     }
 #pragma clang loop unroll(full)
-    for (int d = 0; d < D; ++d) load_tokens(g, t, d, wave, lane, tok[d]);
+    for (int d = 0; d < D; ++d) load_tokens(d, wave, lane, tok[d]);
   }
   // Accumulating into dW: the accumulators start from the old dW values,
   // loaded with the tile's first operand copies (their latency overlaps),
@@ -1311,30 +1327,36 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
     B.commit(Bs, wave, lane);
   }
   // byte offsets of the gathered operand's copies of K tile kt (tokens in tok[0])
-  __device__ __forceinline__ void gather_offsets(const GemmArgs& g, const Tile& t, int kt, int wave,
-                                                 int lane, uint32_t (&gv)[IG]) const {
+  __device__ __forceinline__ void gather_offsets(const GemmArgs& g, int kt, int wave, int lane,
+                                                 uint32_t (&gv)[IG]) const {
     const uint32_t rowb = (uint32_t)g.h * sizeof(T);
-    // branch-free: a row past K or a column past the operand gets bit 31
-    // (kOOB), which puts the offset past the resource (a byte of X or dY is
-    // below 2^31); colb already is kOOB for such a column
+    if ((kt + 1) * OA::BKE <= Ku) {
+      // a whole K tile of the expert's rows (every tile but a partial last one)
 #pragma clang loop unroll(full)
-    for (int i = 0; i < IG; ++i)
-      gv[i] = ((uint32_t)tok[0][i] * rowb + colb[i]) |
-              (k_row(kt, i, wave, lane) >= t.K ? kOOB : 0u);
+      for (int i = 0; i < IG; ++i) gv[i] = (uint32_t)tok[0][i] * rowb + colb[i];
+    } else {
+      // branch-free: a row past K or a column past the operand gets bit 31
+      // (kOOB), which puts the offset past the resource (a byte of X or dY is
+      // below 2^31); colb already is kOOB for such a column
+#pragma clang loop unroll(full)
+      for (int i = 0; i < IG; ++i)
+        gv[i] = ((uint32_t)tok[0][i] * rowb + colb[i]) |
+                (k_row(kt, i, wave, lane) >= Ku ? kOOB : 0u);
+    }
   }
   __device__ __forceinline__ void issue(const GemmArgs& g, const Tile& t, int kt, char* As,
                                         char* Bs, int wave, int lane) {
-    if constexpr (kFC1) gather_offsets(g, t, kt, wave, lane, B.voff);
-    else gather_offsets(g, t, kt, wave, lane, A.voff);
-    if (kFC1) A.rs = plain_rsrc(g, t, kt);
-    else B.rs = plain_rsrc(g, t, kt);
+    if constexpr (kFC1) gather_offsets(g, kt, wave, lane, B.voff);
+    else gather_offsets(g, kt, wave, lane, A.voff);
+    if (kFC1) A.rs = plain_rsrc(g, kt);
+    else B.rs = plain_rsrc(g, kt);
     A.issue(As, 0, wave);
     B.issue(Bs, 0, wave);
 #pragma clang loop unroll(full)
     for (int d = 0; d + 1 < D; ++d)
 #pragma clang loop unroll(full)
       for (int i = 0; i < IG; ++i) tok[d][i] = tok[d + 1][i];
-    load_tokens(g, t, kt + D, wave, lane, tok[D - 1]);  // D tiles ahead
+    load_tokens(kt + D, wave, lane, tok[D - 1]);  // D tiles ahead
   }
   // Vector-memory instructions epilogue() issues: every one, whatever the
   // tile's extent (elements outside it get an offset past the range).
