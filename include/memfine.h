@@ -120,15 +120,34 @@ typedef struct memfine_plan_info {
 } memfine_plan_info;
 
 /*
- * GEMM launch options, for measurements and tests; every setting gives
- * bit-identical results (each output element is one lane's fp32 sum in
- * increasing K order whatever the tiling).  Process-wide; a layer call reads
- * them once when it starts.
+ * Launch options, for measurements and tests.  Every GEMM setting (tile,
+ * raster, split_tail, pair, streams) gives bit-identical results (each
+ * output element is one lane's fp32 sum in increasing K order whatever the
+ * tiling); chunk_order changes the order of the sums that form Y and dX.
+ * Process-wide; a layer call reads them once when it starts, and
+ * memfine_workspace_bytes (hence memfine_plan) follows chunk_order.
  */
 #define MEMFINE_TILE_AUTO    0   /* per problem (the default)                  */
 #define MEMFINE_TILE_128     1   /* 128 x 128 tiles, 4 waves                   */
 #define MEMFINE_TILE_256     2   /* 256 x 256 tiles, 8 waves, direct copies    */
 #define MEMFINE_TILE_256_REG 3   /* 256 x 256 tiles, 8 waves, register-staged  */
+/*
+ * Chunk order.  MEMFINE_CHUNK_TOKENS (the default) is the paper's split,
+ * Eq. (6): chunk i holds the slots of tokens [i T / C, (i + 1) T / C).
+ * MEMFINE_CHUNK_EXPERTS, a variant that is not in the paper: one dispatch
+ * groups all T k slots by expert, and chunk c holds rows [c N / C,
+ * (c + 1) N / C) of that grouping (N = T k), i.e. a run of whole experts
+ * with at most the first and last split.  An expert's weights are then read,
+ * and its fp32 dW written, in one chunk (two for a split expert) instead of
+ * in every chunk; in exchange Y and dX are sums over chunks: the chunk that
+ * holds a token's first row writes its partial sum, later chunks add theirs
+ * to the stored value (one rounding to the storage type per chunk), so
+ * these two outputs are not bit-identical across C or to the token order,
+ * while dW, dgates and the per-chunk peak (at most ceil(N / C) rows plus
+ * the layer's routing tables) follow the same definitions.
+ */
+#define MEMFINE_CHUNK_TOKENS  0
+#define MEMFINE_CHUNK_EXPERTS 1
 typedef struct memfine_launch_options {
   int32_t tile;        /* MEMFINE_TILE_*                                       */
   int32_t raster;      /* -1 per problem; 0 row-major by workgroup id; 1..3
@@ -137,10 +156,12 @@ typedef struct memfine_launch_options {
   int32_t split_tail;  /* 1: a short last round of a GEMM runs as quarter tiles */
   int32_t pair;        /* 1: FC1 dgrad and FC1 wgrad in one launch             */
   int32_t streams;     /* 1: the weight gradients on two side streams          */
+  int32_t chunk_order; /* MEMFINE_CHUNK_* (changes results: see above)         */
 } memfine_launch_options;
 
-/* NULL restores the defaults {AUTO, -1, 1, 0, 0}.  MEMFINE_ERR_INVALID_ARG on
- * a value out of range (the setting is then unchanged). */
+/* NULL restores the defaults {AUTO, -1, 1, 0, 0, TOKENS}.
+ * MEMFINE_ERR_INVALID_ARG on a value out of range (the setting is then
+ * unchanged). */
 int memfine_set_launch_options(const memfine_launch_options* opts);
 int memfine_get_launch_options(memfine_launch_options* opts_out);
 
@@ -207,8 +228,9 @@ int memfine_plan(const memfine_shape* shape, const int64_t* h_counts, int64_t bu
  * Bytes of working memory the layer allocates for its largest chunk (the
  * per-chunk buffers of memfine_moe_fwd or memfine_moe_bwd, pass =
  * MEMFINE_PASS_FWD / MEMFINE_PASS_BWD) - the activation peak of the chunked
- * layer that Section 4.1 says replaces the unchunked one.  Returns < 0 on
- * invalid arguments.
+ * layer that Section 4.1 says replaces the unchunked one.  Under
+ * MEMFINE_CHUNK_EXPERTS it adds the layer's routing tables, held for the
+ * whole call.  Returns < 0 on invalid arguments.
  */
 int64_t memfine_workspace_bytes(const memfine_shape* shape, int32_t chunks, int32_t pass);
 

@@ -3,7 +3,7 @@
 The compute lives in libmemfine.so (hand-written gfx950 HIP kernels behind
 the C ABI of include/memfine.h); this package only builds and binds it.
 """
-from ._lib import (BF16, ERR_SCRATCH, F32, NOALLOC_SCRATCH_BYTES, PASS_BWD, PASS_FWD, TILE_128, TILE_256, TILE_256_REG,  # noqa: F401
+from ._lib import (BF16, CHUNK_EXPERTS, CHUNK_TOKENS, ERR_SCRATCH, F32, NOALLOC_SCRATCH_BYTES, PASS_BWD, PASS_FWD, TILE_128, TILE_256, TILE_256_REG,  # noqa: F401
                    TILE_AUTO, MemfineError, TorchAllocator, lib, make_model, make_shape,
                    memfine_activation_memory, memfine_count, memfine_dispatch,
                    memfine_get_launch_options, memfine_mact_select, memfine_mact_thresholds,

@@ -57,14 +57,15 @@ class PlanInfo(ctypes.Structure):
 
 
 TILE_AUTO, TILE_128, TILE_256, TILE_256_REG = 0, 1, 2, 3
+CHUNK_TOKENS, CHUNK_EXPERTS = 0, 1
 
 
 class LaunchOptions(ctypes.Structure):
     """memfine_launch_options: GEMM tile shape, tile order, split tail, paired
-    FC1 backward launch, side streams (all bit-identical)."""
+    FC1 backward launch, side streams (all bit-identical), chunk order."""
     _fields_ = [("tile", ctypes.c_int32), ("raster", ctypes.c_int32),
                 ("split_tail", ctypes.c_int32), ("pair", ctypes.c_int32),
-                ("streams", ctypes.c_int32)]
+                ("streams", ctypes.c_int32), ("chunk_order", ctypes.c_int32)]
 
 
 class Model(ctypes.Structure):
@@ -374,9 +375,10 @@ def memfine_pool_high_water(reset: bool = False) -> int:
 
 
 def memfine_set_launch_options(tile: int = TILE_AUTO, raster: int = -1, split_tail: bool = True,
-                               pair: bool = False, streams: bool = False) -> None:
+                               pair: bool = False, streams: bool = False,
+                               chunk_order: int = CHUNK_TOKENS) -> None:
     o = LaunchOptions(int(tile), int(raster), int(bool(split_tail)), int(bool(pair)),
-                      int(bool(streams)))
+                      int(bool(streams)), int(chunk_order))
     _check(lib().memfine_set_launch_options(ctypes.byref(o)), "memfine_set_launch_options")
 
 

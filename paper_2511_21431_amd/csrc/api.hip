@@ -77,6 +77,7 @@ struct Layout {
     kA, kY,                 // forward
     kU, kAg, kDxp, kDgp,    // backward
     kCtr,                   // backward: tile counters of the two weight gradients
+    kOffC, kOrderC, kWexp, kWmode,  // expert-ordered chunks: the current chunk's view
     kNum
   };
   int64_t off[kNum];
@@ -86,23 +87,34 @@ struct Layout {
 
 int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 
-void chunk_layout(const memfine_shape& s, int64_t n, int pass, Layout& L) {
+// Buffers for n slots: the routing tables of one dispatch (`tables`), the
+// views of expert-ordered chunks (`views`), and the intermediates of a
+// forward or backward pass over n rows (`pass`, or -1 for none).
+void layout(const memfine_shape& s, int64_t n, int pass, bool tables, bool views, Layout& L) {
   const int64_t es = elem_bytes(s), E = s.E, nb = dispatch_blocks(n);
   const int64_t P = dgate_partials(s.F);
   for (int i = 0; i < Layout::kNum; ++i) L.size[i] = 0;
-  L.size[Layout::kBcount] = E * nb * 4;
-  L.size[Layout::kBstart] = E * nb * 4;
-  L.size[Layout::kCounts] = E * 4;
-  L.size[Layout::kOffsets] = (E + 1) * 4;
-  L.size[Layout::kOrder] = E * 4;
-  L.size[Layout::kSorted] = n * 4;
-  L.size[Layout::kRowOf] = n * 4;
-  L.size[Layout::kTokOf] = n * 4;
-  L.size[Layout::kGateOf] = n * 4;
+  if (tables) {
+    L.size[Layout::kBcount] = E * nb * 4;
+    L.size[Layout::kBstart] = E * nb * 4;
+    L.size[Layout::kCounts] = E * 4;
+    L.size[Layout::kOffsets] = (E + 1) * 4;
+    L.size[Layout::kOrder] = E * 4;
+    L.size[Layout::kSorted] = n * 4;
+    L.size[Layout::kRowOf] = n * 4;
+    L.size[Layout::kTokOf] = n * 4;
+    L.size[Layout::kGateOf] = n * 4;
+  }
+  if (views) {
+    L.size[Layout::kOffC] = (E + 1) * 4;
+    L.size[Layout::kOrderC] = E * 4;
+    L.size[Layout::kWexp] = 4;
+    L.size[Layout::kWmode] = E * 4;
+  }
   if (pass == MEMFINE_PASS_FWD) {
     L.size[Layout::kA] = n * s.F * es;
     L.size[Layout::kY] = n * s.h * es;
-  } else {
+  } else if (pass == MEMFINE_PASS_BWD) {
     L.size[Layout::kU] = n * 2 * s.F * es;
     L.size[Layout::kAg] = n * s.F * es;
     L.size[Layout::kDxp] = n * s.h * es;
@@ -115,6 +127,10 @@ void chunk_layout(const memfine_shape& s, int64_t n, int pass, Layout& L) {
     o += align256(L.size[i]);
   }
   L.total = o;
+}
+// a token-range chunk of n slots: its dispatch tables and its pass buffers
+void chunk_layout(const memfine_shape& s, int64_t n, int pass, Layout& L) {
+  layout(s, n, pass, true, false, L);
 }
 
 // tokens in the largest chunk of the floor-balanced split of T into C
@@ -231,6 +247,7 @@ struct ChunkBuffers {
   void *a, *y, *u, *ag, *dxp;
   float* dgp;
   int32_t* ctr;  // [2] tile counters: FC1 wgrad, FC2 wgrad
+  int32_t *off_c, *order_c, *wexp, *wmode;  // expert-ordered chunks: the chunk's view
 };
 
 ChunkBuffers carve(void* base, const Layout& L) {
@@ -252,6 +269,10 @@ ChunkBuffers carve(void* base, const Layout& L) {
   c.dxp = b + L.off[Layout::kDxp];
   c.dgp = (float*)(b + L.off[Layout::kDgp]);
   c.ctr = (int32_t*)(b + L.off[Layout::kCtr]);
+  c.off_c = (int32_t*)(b + L.off[Layout::kOffC]);
+  c.order_c = (int32_t*)(b + L.off[Layout::kOrderC]);
+  c.wexp = (int32_t*)(b + L.off[Layout::kWexp]);
+  c.wmode = (int32_t*)(b + L.off[Layout::kWmode]);
   return c;
 }
 
@@ -259,7 +280,8 @@ ChunkBuffers carve(void* base, const Layout& L) {
 // copied under a lock at the start of every layer call, so that a call never
 // sees a half-written update.  The defaults are the measured-best choices.
 std::mutex g_opts_mu;
-memfine_launch_options g_opts = {MEMFINE_TILE_AUTO, -1, 1, 0, 0};
+const memfine_launch_options kDefaultOptions = {MEMFINE_TILE_AUTO, -1, 1, 0, 0, MEMFINE_CHUNK_TOKENS};
+memfine_launch_options g_opts = kDefaultOptions;
 
 memfine_launch_options launch_options() {
   std::lock_guard<std::mutex> lk(g_opts_mu);
@@ -410,7 +432,39 @@ int scratch_address(void** out) {
 
 int moe_fwd_impl(const memfine_shape* shape, int32_t chunks, const void* d_X,
                  const int32_t* d_idx, const float* d_gates, const void* d_W1, const void* d_W2,
-                 void* d_Y, const memfine_allocator* alloc, void* fixed_ws, void* stream);
+                 void* d_Y, const memfine_allocator* alloc, void* fixed_ws,
+                 const memfine_launch_options& opt, void* stream);
+
+// Expert-ordered chunks (launch option chunk_order): one dispatch groups all
+// T k slots by expert; chunk c is rows [c N / C, (c + 1) N / C) of that
+// order.  Its routing tables and the chunk views live for the whole call.
+int64_t expert_meta_bytes(const memfine_shape& s) {
+  Layout L;
+  layout(s, s.T * (int64_t)s.k, -1, true, true, L);
+  return L.total;
+}
+int64_t expert_chunks(const memfine_shape& s, int32_t chunks) {
+  return std::min<int64_t>(chunks, s.T);
+}
+int64_t expert_chunk_row(const memfine_shape& s, int64_t C, int64_t c) {
+  return c * (s.T * (int64_t)s.k) / C;
+}
+
+int64_t workspace_bytes(const memfine_shape& s, int32_t chunks, int32_t pass, int32_t order) {
+  if (order == MEMFINE_CHUNK_EXPERTS) {
+    const int64_t N = s.T * (int64_t)s.k;
+    if (N == 0) return 0;
+    const int64_t C = expert_chunks(s, chunks);
+    Layout L;
+    layout(s, (N + C - 1) / C, pass, false, false, L);
+    return expert_meta_bytes(s) + L.total;
+  }
+  const int64_t n = max_chunk_tokens(s.T, chunks) * s.k;
+  if (n == 0) return 0;
+  Layout L;
+  chunk_layout(s, n, pass, L);
+  return L.total;
+}
 
 }  // namespace
 
@@ -493,11 +547,12 @@ int memfine_plan(const memfine_shape* shape, const int64_t* h_counts, int64_t bu
 }
 
 int memfine_set_launch_options(const memfine_launch_options* opts) {
-  memfine_launch_options o = {MEMFINE_TILE_AUTO, -1, 1, 0, 0};
+  memfine_launch_options o = kDefaultOptions;
   if (opts) {
     if (opts->tile < MEMFINE_TILE_AUTO || opts->tile > MEMFINE_TILE_256_REG ||
         opts->raster < -1 || opts->raster > 4 || (opts->split_tail != 0 && opts->split_tail != 1) ||
-        (opts->pair != 0 && opts->pair != 1) || (opts->streams != 0 && opts->streams != 1))
+        (opts->pair != 0 && opts->pair != 1) || (opts->streams != 0 && opts->streams != 1) ||
+        (opts->chunk_order != MEMFINE_CHUNK_TOKENS && opts->chunk_order != MEMFINE_CHUNK_EXPERTS))
       return MEMFINE_ERR_INVALID_ARG;
     o = *opts;
   }
@@ -572,11 +627,7 @@ int64_t memfine_workspace_bytes(const memfine_shape* shape, int32_t chunks, int3
   if (check_shape(shape)) return MEMFINE_ERR_INVALID_ARG;
   if (chunks < 1 || (pass != MEMFINE_PASS_FWD && pass != MEMFINE_PASS_BWD))
     return MEMFINE_ERR_INVALID_ARG;
-  const int64_t n = max_chunk_tokens(shape->T, chunks) * shape->k;
-  if (n == 0) return 0;
-  Layout L;
-  chunk_layout(*shape, n, pass, L);
-  return L.total;
+  return workspace_bytes(*shape, chunks, pass, launch_options().chunk_order);
 }
 
 int memfine_count(const memfine_shape* shape, const int32_t* d_idx, int32_t* d_work,
@@ -648,7 +699,8 @@ int memfine_dispatch(const memfine_shape* shape, const int32_t* d_idx, int64_t t
 int memfine_moe_fwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
                     const int32_t* d_idx, const float* d_gates, const void* d_W1,
                     const void* d_W2, void* d_Y, const memfine_allocator* alloc, void* stream) {
-  return moe_fwd_impl(shape, chunks, d_X, d_idx, d_gates, d_W1, d_W2, d_Y, alloc, nullptr, stream);
+  return moe_fwd_impl(shape, chunks, d_X, d_idx, d_gates, d_W1, d_W2, d_Y, alloc, nullptr,
+                      launch_options(), stream);
 }
 
 int memfine_moe_fwd_noalloc(const memfine_shape* shape, int32_t chunks, const void* d_X,
@@ -657,14 +709,16 @@ int memfine_moe_fwd_noalloc(const memfine_shape* shape, int32_t chunks, const vo
   int rc = check_shape(shape);
   if (rc) return rc;
   if (chunks < 1) return MEMFINE_ERR_INVALID_ARG;
-  if (memfine_workspace_bytes(shape, chunks, MEMFINE_PASS_FWD) > kScratchBytes)
+  // one copy of the options for the size check and the call
+  const memfine_launch_options opt = launch_options();
+  if (workspace_bytes(*shape, chunks, MEMFINE_PASS_FWD, opt.chunk_order) > kScratchBytes)
     return MEMFINE_ERR_SCRATCH;
   if (shape->T == 0) return MEMFINE_OK;
   void* scratch_dev = nullptr;
   rc = scratch_address(&scratch_dev);
   if (rc) return rc;
   return moe_fwd_impl(shape, chunks, d_X, d_idx, d_gates, d_W1, d_W2, d_Y, nullptr, scratch_dev,
-                      stream);
+                      opt, stream);
 }
 
 }  // extern "C"
@@ -673,9 +727,126 @@ namespace {
 // The chunked forward.  Each chunk's buffers come from `fixed_ws` when it is
 // not null (it then holds the largest chunk's workspace; nothing is
 // allocated or released), else from ws_alloc / ws_release.
+// Profiling of expert-ordered chunks: a host copy of the layer's expert
+// offsets (one synchronisation per call, only while kernel timing is on),
+// for the algorithmic bytes of each chunk's launches.
+std::vector<int32_t> offsets_for_profile(const int32_t* d_offsets, int E, hipStream_t s) {
+  std::vector<int32_t> h;
+  if (g_prof_mask == 0) return h;
+  h.resize(E + 1);
+  if (hipMemcpyAsync(h.data(), d_offsets, (E + 1) * sizeof(int32_t), hipMemcpyDeviceToHost, s) !=
+          hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess) {
+    (void)hipGetLastError();
+    h.clear();
+  }
+  return h;
+}
+// experts with rows in [p0, p1), and those of them whose dW the chunk adds to
+struct ChunkExperts {
+  double in = 0, add = 0;
+};
+ChunkExperts chunk_experts(const std::vector<int32_t>& off, int E, int64_t p0, int64_t p1,
+                           bool accumulate) {
+  ChunkExperts c;
+  if (off.empty()) {  // unknown: every expert, read and written
+    c.in = c.add = E;
+    return c;
+  }
+  for (int e = 0; e < E; ++e) {
+    const int64_t lo = off[e], hi = off[e + 1];
+    if (std::min(hi, p1) > std::max(lo, p0)) {
+      c.in += 1;
+      if (accumulate || lo < p0) c.add += 1;
+    }
+  }
+  return c;
+}
+
+// The expert-ordered forward: the layer's dispatch, then per chunk its view,
+// FC1 and FC2 over its rows, and the combine of its rows into Y.  With
+// `fixed_ws` the tables and the chunk buffers are carved from it.
+int moe_fwd_experts(const memfine_shape& S, int32_t chunks, const void* d_X, const int32_t* d_idx,
+                    const float* d_gates, const void* d_W1, const void* d_W2, void* d_Y,
+                    const memfine_allocator* alloc, void* fixed_ws,
+                    const memfine_launch_options& opt, hipStream_t s) {
+  const int64_t N = S.T * (int64_t)S.k, C = expert_chunks(S, chunks);
+  const double es = (double)elem_bytes(S), hF = (double)S.h * S.F;
+  Layout Lm;
+  layout(S, N, -1, true, true, Lm);
+  Layout Lmax;
+  layout(S, (N + C - 1) / C, MEMFINE_PASS_FWD, false, false, Lmax);
+  // The first chunk's buffers are taken before the tables, so that with the
+  // library's own allocator the chunks reuse the stream's cached block.
+  void* ws = fixed_ws ? (char*)fixed_ws + Lm.total : ws_alloc(alloc, (size_t)Lmax.total, s);
+  if (!ws) return MEMFINE_ERR_OOM;
+  void* meta = fixed_ws ? fixed_ws : ws_alloc(alloc, (size_t)Lm.total, s);
+  if (!meta) {
+    if (!fixed_ws) ws_release(alloc, ws, (size_t)Lmax.total, s);
+    return MEMFINE_ERR_OOM;
+  }
+  const ChunkBuffers mb = carve(meta, Lm);
+  hipError_t err;
+  {
+    KernelTimer kt(MEMFINE_K_DISPATCH, s, 0.0, dispatch_work(N).bytes);
+    err = launch_dispatch(d_idx, d_gates, 0, (int)N, S.E, S.k, mb.m, s);
+  }
+  const std::vector<int32_t> hoff =
+      err == hipSuccess ? offsets_for_profile(mb.m.offsets, S.E, s) : std::vector<int32_t>();
+  for (int64_t c = 0; c < C && err == hipSuccess; ++c) {
+    const int64_t p0 = expert_chunk_row(S, C, c), p1 = expert_chunk_row(S, C, c + 1);
+    const int64_t n = p1 - p0;
+    if (n == 0) continue;
+    Layout L;
+    layout(S, n, MEMFINE_PASS_FWD, false, false, L);
+    if (!ws) ws = ws_alloc(alloc, (size_t)Lmax.total, s);
+    if (!ws) {
+      ws_release(alloc, meta, (size_t)Lm.total, s);
+      return MEMFINE_ERR_OOM;
+    }
+    const ChunkBuffers cb = carve(ws, L);
+    err = launch_chunk_view(mb.m.offsets, S.E, (int)p0, (int)p1, c == 0, 0, mb.off_c, mb.order_c,
+                            mb.wexp, mb.wmode, s);
+    GemmArgs g = gemm_args(S, n, cb, opt);
+    g.offsets = mb.off_c;
+    g.order = mb.order_c;
+    g.tok_of_row = mb.m.tok_of_row + p0;
+    g.gate_of_row = mb.m.gate_of_row + p0;
+    g.X = d_X;
+    g.W1 = d_W1;
+    g.W2 = d_W2;
+    const double nd = (double)n, Ec = chunk_experts(hoff, S.E, p0, p1, false).in;
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC1, s, 4.0 * nd * hF, es * (nd * S.h + 2.0 * Ec * hF + nd * S.F));
+      err = launch_fc1_fwd(g, s);
+    }
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC2, s, 2.0 * nd * hF, es * (nd * S.F + Ec * hF + nd * S.h));
+      err = launch_fc2_fwd(g, s);
+    }
+    if (err == hipSuccess) {
+      // the chunk's rows once, and a read and write of (at most) one Y row each
+      KernelTimer kt(MEMFINE_K_COMBINE, s, 2.0 * nd * S.h,
+                     es * 3.0 * nd * S.h + 4.0 * (double)N + 4.0 * nd);
+      err = launch_combine_rows(S.dtype, cb.y, mb.m.row_of_slot, d_gates, S.T, S.h, S.k, (int)p0,
+                                (int)p1, d_Y, s);
+    }
+    if (!fixed_ws) {  // the chunk's buffers go back before the next chunk takes its own
+      ws_release(alloc, ws, (size_t)Lmax.total, s);
+      ws = nullptr;
+    }
+  }
+  if (!fixed_ws) {
+    if (ws) ws_release(alloc, ws, (size_t)Lmax.total, s);
+    ws_release(alloc, meta, (size_t)Lm.total, s);
+  }
+  return err == hipSuccess ? MEMFINE_OK : MEMFINE_ERR_HIP;
+}
+
 int moe_fwd_impl(const memfine_shape* shape, int32_t chunks, const void* d_X,
                  const int32_t* d_idx, const float* d_gates, const void* d_W1, const void* d_W2,
-                 void* d_Y, const memfine_allocator* alloc, void* fixed_ws, void* stream) {
+                 void* d_Y, const memfine_allocator* alloc, void* fixed_ws,
+                 const memfine_launch_options& opt, void* stream) {
   int rc = check_shape(shape);
   if (rc) return rc;
   if (chunks < 1) return MEMFINE_ERR_INVALID_ARG;
@@ -683,9 +854,11 @@ int moe_fwd_impl(const memfine_shape* shape, int32_t chunks, const void* d_X,
   if (S.T == 0) return MEMFINE_OK;
   if (!d_X || !d_idx || !d_gates || !d_W1 || !d_W2 || !d_Y) return MEMFINE_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
+  if (opt.chunk_order == MEMFINE_CHUNK_EXPERTS)
+    return moe_fwd_experts(S, chunks, d_X, d_idx, d_gates, d_W1, d_W2, d_Y, alloc, fixed_ws, opt,
+                           s);
   const int64_t C = std::min<int64_t>(chunks, S.T);
   const double es = (double)elem_bytes(S);
-  const memfine_launch_options opt = launch_options();
   for (int64_t i = 0; i < C; ++i) {
     const int64_t t0 = i * S.T / C, t1 = (i + 1) * S.T / C;
     const int64_t tokens = t1 - t0, n = tokens * S.k;
@@ -727,6 +900,183 @@ int moe_fwd_impl(const memfine_shape* shape, int32_t chunks, const void* d_X,
 }
 }  // namespace
 
+namespace {
+// Algorithmic work of a chunk's backward GEMMs (flops, bytes).
+struct BwdWork {
+  Work fc2d, rec, fc2w, fc1w, fc1d;
+};
+// A chunk's backward GEMMs, after its dispatch: FC2 dgrad, the FC1
+// recomputation with the SwiGLU backward, the two weight gradients and the
+// FC1 dgrad (the last three on side streams, or in one launch, as the
+// launch options say).
+hipError_t bwd_gemms(const GemmArgs& g, const ChunkBuffers& cb, const memfine_launch_options& opt,
+                     const BwdWork& w, hipStream_t s) {
+  hipError_t err;
+  {  // dA = dY W2 of the chunk's rows (into ag)
+    KernelTimer kt(MEMFINE_K_FC2_DGRAD, s, w.fc2d.flops, w.fc2d.bytes);
+    err = launch_fc2_dgrad(g, s);
+  }
+  if (err == hipSuccess) {  // recompute F_w(X_i)'s FC1; SwiGLU backward: du, g * a, dg partials
+    KernelTimer kt(MEMFINE_K_FC1_RECOMP, s, w.rec.flops, w.rec.bytes);
+    err = launch_fc1_recompute(g, s);
+  }
+  SideStreams* ss = (!opt.pair && opt.streams) ? side_streams() : nullptr;
+  if (ss) {
+    // The two weight gradients and the FC1 dgrad read what the recompute
+    // wrote and write disjoint outputs (dW1, dW2, the chunk's dX rows).
+    // The weight gradients run on side streams beside the dgrad, so that
+    // their dW read-modify-write phases overlap the dgrad's matrix work;
+    // the caller's stream joins them before the unpermute (and before
+    // the chunk's buffers are released, also after an error).
+    std::lock_guard<std::mutex> lk(ss->mu);
+    bool forked = false;
+    if (err == hipSuccess) err = hipEventRecord(ss->fork, s);
+    if (err == hipSuccess) {
+      forked = true;
+      for (int j = 0; j < 2 && err == hipSuccess; ++j) err = hipStreamWaitEvent(ss->s[j], ss->fork, 0);
+    }
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC1_WGRAD, ss->s[0], w.fc1w.flops, w.fc1w.bytes);
+      GemmArgs gw = g;
+      gw.tile_ctr = cb.ctr;
+      err = launch_fc1_wgrad(gw, ss->s[0]);
+    }
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC2_WGRAD, ss->s[1], w.fc2w.flops, w.fc2w.bytes);
+      GemmArgs gw = g;
+      gw.tile_ctr = cb.ctr + 1;
+      err = launch_fc2_wgrad(gw, ss->s[1]);
+    }
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC1_DGRAD, s, w.fc1d.flops, w.fc1d.bytes);
+      err = launch_fc1_dgrad(g, s);
+    }
+    if (forked) {
+      for (int j = 0; j < 2; ++j) {
+        const hipError_t e1 = hipEventRecord(ss->join[j], ss->s[j]);
+        const hipError_t e2 = e1 == hipSuccess ? hipStreamWaitEvent(s, ss->join[j], 0) : e1;
+        if (e2 != hipSuccess) {
+          // the caller's stream cannot be ordered after the side stream:
+          // wait for it on the host before the buffers are released
+          (void)hipStreamSynchronize(ss->s[j]);
+          if (err == hipSuccess) err = e2;
+        }
+      }
+    }
+    return err;
+  }
+  if (err == hipSuccess) {
+    KernelTimer kt(MEMFINE_K_FC2_WGRAD, s, w.fc2w.flops, w.fc2w.bytes);
+    GemmArgs gw = g;
+    gw.tile_ctr = cb.ctr + 1;
+    err = launch_fc2_wgrad(gw, s);
+  }
+  if (opt.pair) {
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC1_BWD, s, w.fc1d.flops + w.fc1w.flops,
+                     w.fc1d.bytes + w.fc1w.bytes);
+      err = launch_fc1_dgrad_wgrad(g, s);
+    }
+  } else {
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC1_WGRAD, s, w.fc1w.flops, w.fc1w.bytes);
+      GemmArgs gw = g;
+      gw.tile_ctr = cb.ctr;
+      err = launch_fc1_wgrad(gw, s);
+    }
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_FC1_DGRAD, s, w.fc1d.flops, w.fc1d.bytes);
+      err = launch_fc1_dgrad(g, s);
+    }
+  }
+  return err;
+}
+
+// The expert-ordered backward: the layer's dispatch, then per chunk its view
+// (with each expert's dW mode: the chunk holding an expert's first rows
+// overwrites its dW unless the caller accumulates, later chunks add), the
+// backward GEMMs over its rows, and the unpermute of its rows into dX.
+int moe_bwd_experts(const memfine_shape& S, int32_t chunks, const void* d_X, const int32_t* d_idx,
+                    const float* d_gates, const void* d_W1, const void* d_W2, const void* d_dY,
+                    void* d_dX, float* d_dW1, float* d_dW2, float* d_dgates,
+                    int32_t accumulate_dW, const memfine_allocator* alloc,
+                    const memfine_launch_options& opt, hipStream_t s) {
+  const int64_t N = S.T * (int64_t)S.k, C = expert_chunks(S, chunks);
+  const double es = (double)elem_bytes(S), hF = (double)S.h * S.F;
+  Layout Lm;
+  layout(S, N, -1, true, true, Lm);
+  Layout Lmax;
+  layout(S, (N + C - 1) / C, MEMFINE_PASS_BWD, false, false, Lmax);
+  // the first chunk's buffers before the tables (as in the forward)
+  void* ws = ws_alloc(alloc, (size_t)Lmax.total, s);
+  if (!ws) return MEMFINE_ERR_OOM;
+  void* meta = ws_alloc(alloc, (size_t)Lm.total, s);
+  if (!meta) {
+    ws_release(alloc, ws, (size_t)Lmax.total, s);
+    return MEMFINE_ERR_OOM;
+  }
+  const ChunkBuffers mb = carve(meta, Lm);
+  hipError_t err;
+  {
+    KernelTimer kt(MEMFINE_K_DISPATCH, s, 0.0, dispatch_work(N).bytes);
+    err = launch_dispatch(d_idx, d_gates, 0, (int)N, S.E, S.k, mb.m, s);
+  }
+  const std::vector<int32_t> hoff =
+      err == hipSuccess ? offsets_for_profile(mb.m.offsets, S.E, s) : std::vector<int32_t>();
+  for (int64_t c = 0; c < C && err == hipSuccess; ++c) {
+    const int64_t p0 = expert_chunk_row(S, C, c), p1 = expert_chunk_row(S, C, c + 1);
+    const int64_t n = p1 - p0;
+    if (n == 0) continue;
+    Layout L;
+    layout(S, n, MEMFINE_PASS_BWD, false, false, L);
+    if (!ws) ws = ws_alloc(alloc, (size_t)Lmax.total, s);
+    if (!ws) {
+      ws_release(alloc, meta, (size_t)Lm.total, s);
+      return MEMFINE_ERR_OOM;
+    }
+    const ChunkBuffers cb = carve(ws, L);
+    err = launch_chunk_view(mb.m.offsets, S.E, (int)p0, (int)p1, c == 0, accumulate_dW, mb.off_c,
+                            mb.order_c, mb.wexp, mb.wmode, s);
+    GemmArgs g = gemm_args(S, n, cb, opt);
+    g.offsets = mb.off_c;
+    g.order = mb.order_c;
+    g.tok_of_row = mb.m.tok_of_row + p0;
+    g.gate_of_row = mb.m.gate_of_row + p0;
+    g.wmode = mb.wmode;
+    g.wexperts = mb.wexp;
+    g.accumulate = accumulate_dW;
+    g.X = d_X;
+    g.dY = d_dY;
+    g.W1 = d_W1;
+    g.W2 = d_W2;
+    g.dW1 = d_dW1;
+    g.dW2 = d_dW2;
+    const ChunkExperts ce = chunk_experts(hoff, S.E, p0, p1, accumulate_dW != 0);
+    const double nd = (double)n;
+    // dW: every element of the chunk's experts written, and read where added
+    const double dw = 4.0 * ce.in + 4.0 * ce.add;
+    const BwdWork w = {
+        {2.0 * nd * hF, es * (nd * S.h + ce.in * hF + nd * S.F)},
+        {4.0 * nd * hF, es * (nd * S.h + 2.0 * ce.in * hF + 4.0 * nd * S.F) + 4.0 * nd * g.P},
+        {2.0 * nd * hF, es * (nd * S.h + nd * S.F) + dw * hF},
+        {4.0 * nd * hF, es * (2.0 * nd * S.F + nd * S.h) + 2.0 * dw * hF},
+        {4.0 * nd * hF, es * (2.0 * nd * S.F + 2.0 * ce.in * hF + nd * S.h)}};
+    if (err == hipSuccess) err = bwd_gemms(g, cb, opt, w, s);
+    if (err == hipSuccess) {
+      KernelTimer kt(MEMFINE_K_UNPERMUTE, s, nd * S.h,
+                     es * 3.0 * nd * S.h + 4.0 * (double)N + 4.0 * nd * (g.P + 1));
+      err = launch_unpermute_rows(S.dtype, cb.dxp, cb.dgp, g.P, mb.m.row_of_slot, S.T, S.h, S.k,
+                                  (int)p0, (int)p1, d_dX, d_dgates, s);
+    }
+    ws_release(alloc, ws, (size_t)Lmax.total, s);
+    ws = nullptr;
+  }
+  if (ws) ws_release(alloc, ws, (size_t)Lmax.total, s);
+  ws_release(alloc, meta, (size_t)Lm.total, s);
+  return err == hipSuccess ? MEMFINE_OK : MEMFINE_ERR_HIP;
+}
+}  // namespace
+
 extern "C" {
 
 int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
@@ -752,8 +1102,11 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
     if (err == hipSuccess) err = launch_fill_i32((int32_t*)d_dW2, w2, 0, s);
     return hip_status(err);
   }
-  const int64_t C = std::min<int64_t>(chunks, S.T);
   const memfine_launch_options opt = launch_options();
+  if (opt.chunk_order == MEMFINE_CHUNK_EXPERTS)
+    return moe_bwd_experts(S, chunks, d_X, d_idx, d_gates, d_W1, d_W2, d_dY, d_dX, d_dW1, d_dW2,
+                           d_dgates, accumulate_dW, alloc, opt, s);
+  const int64_t C = std::min<int64_t>(chunks, S.T);
   bool first = true;
   for (int64_t i = 0; i < C; ++i) {
     const int64_t t0 = i * S.T / C, t1 = (i + 1) * S.T / C;
@@ -779,90 +1132,13 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
       KernelTimer kt(MEMFINE_K_DISPATCH, s, 0.0, dispatch_work(n).bytes);
       err = launch_dispatch(d_idx, d_gates, t0 * S.k, (int)n, S.E, S.k, cb.m, s);
     }
-    // algorithmic work of the backward GEMMs (flops, bytes)
-    const Work w_fc2d = {2.0 * nd * hF, es * (td * S.h + Ed * hF + nd * S.F)};
-    const Work w_rec = {4.0 * nd * hF,
-                        es * (td * S.h + 2.0 * Ed * hF + 4.0 * nd * S.F) + 4.0 * nd * g.P};
-    const Work w_fc2w = {2.0 * nd * hF, es * (td * S.h + nd * S.F) + dw_rmw * Ed * hF};
-    const Work w_fc1w = {4.0 * nd * hF, es * (2.0 * nd * S.F + td * S.h) + 2.0 * dw_rmw * Ed * hF};
-    const Work w_fc1d = {4.0 * nd * hF, es * (2.0 * nd * S.F + 2.0 * Ed * hF + nd * S.h)};
-    if (err == hipSuccess) {  // dA = dY W2 of the chunk's rows (into ag)
-      KernelTimer kt(MEMFINE_K_FC2_DGRAD, s, w_fc2d.flops, w_fc2d.bytes);
-      err = launch_fc2_dgrad(g, s);
-    }
-    if (err == hipSuccess) {  // recompute F_w(X_i)'s FC1; SwiGLU backward: du, g * a, dg partials
-      KernelTimer kt(MEMFINE_K_FC1_RECOMP, s, w_rec.flops, w_rec.bytes);
-      err = launch_fc1_recompute(g, s);
-    }
-    SideStreams* ss = (!opt.pair && opt.streams) ? side_streams() : nullptr;
-    if (ss) {
-      // The two weight gradients and the FC1 dgrad read what the recompute
-      // wrote and write disjoint outputs (dW1, dW2, the chunk's dX rows).
-      // The weight gradients run on side streams beside the dgrad, so that
-      // their dW read-modify-write phases overlap the dgrad's matrix work;
-      // the caller's stream joins them before the unpermute (and before
-      // the chunk's buffers are released, also after an error).
-      std::lock_guard<std::mutex> lk(ss->mu);
-      bool forked = false;
-      if (err == hipSuccess) err = hipEventRecord(ss->fork, s);
-      if (err == hipSuccess) {
-        forked = true;
-        for (int j = 0; j < 2 && err == hipSuccess; ++j) err = hipStreamWaitEvent(ss->s[j], ss->fork, 0);
-      }
-      if (err == hipSuccess) {
-        KernelTimer kt(MEMFINE_K_FC1_WGRAD, ss->s[0], w_fc1w.flops, w_fc1w.bytes);
-        GemmArgs gw = g;
-        gw.tile_ctr = cb.ctr;
-        err = launch_fc1_wgrad(gw, ss->s[0]);
-      }
-      if (err == hipSuccess) {
-        KernelTimer kt(MEMFINE_K_FC2_WGRAD, ss->s[1], w_fc2w.flops, w_fc2w.bytes);
-        GemmArgs gw = g;
-        gw.tile_ctr = cb.ctr + 1;
-        err = launch_fc2_wgrad(gw, ss->s[1]);
-      }
-      if (err == hipSuccess) {
-        KernelTimer kt(MEMFINE_K_FC1_DGRAD, s, w_fc1d.flops, w_fc1d.bytes);
-        err = launch_fc1_dgrad(g, s);
-      }
-      if (forked) {
-        for (int j = 0; j < 2; ++j) {
-          const hipError_t e1 = hipEventRecord(ss->join[j], ss->s[j]);
-          const hipError_t e2 = e1 == hipSuccess ? hipStreamWaitEvent(s, ss->join[j], 0) : e1;
-          if (e2 != hipSuccess) {
-            // the caller's stream cannot be ordered after the side stream:
-            // wait for it on the host before the buffers are released
-            (void)hipStreamSynchronize(ss->s[j]);
-            if (err == hipSuccess) err = e2;
-          }
-        }
-      }
-    } else {
-      if (err == hipSuccess) {
-        KernelTimer kt(MEMFINE_K_FC2_WGRAD, s, w_fc2w.flops, w_fc2w.bytes);
-        GemmArgs gw = g;
-        gw.tile_ctr = cb.ctr + 1;
-        err = launch_fc2_wgrad(gw, s);
-      }
-      if (opt.pair) {
-        if (err == hipSuccess) {
-          KernelTimer kt(MEMFINE_K_FC1_BWD, s, w_fc1d.flops + w_fc1w.flops,
-                         w_fc1d.bytes + w_fc1w.bytes);
-          err = launch_fc1_dgrad_wgrad(g, s);
-        }
-      } else {
-        if (err == hipSuccess) {
-          KernelTimer kt(MEMFINE_K_FC1_WGRAD, s, w_fc1w.flops, w_fc1w.bytes);
-          GemmArgs gw = g;
-          gw.tile_ctr = cb.ctr;
-          err = launch_fc1_wgrad(gw, s);
-        }
-        if (err == hipSuccess) {
-          KernelTimer kt(MEMFINE_K_FC1_DGRAD, s, w_fc1d.flops, w_fc1d.bytes);
-          err = launch_fc1_dgrad(g, s);
-        }
-      }
-    }
+    const BwdWork w = {
+        {2.0 * nd * hF, es * (td * S.h + Ed * hF + nd * S.F)},
+        {4.0 * nd * hF, es * (td * S.h + 2.0 * Ed * hF + 4.0 * nd * S.F) + 4.0 * nd * g.P},
+        {2.0 * nd * hF, es * (td * S.h + nd * S.F) + dw_rmw * Ed * hF},
+        {4.0 * nd * hF, es * (2.0 * nd * S.F + td * S.h) + 2.0 * dw_rmw * Ed * hF},
+        {4.0 * nd * hF, es * (2.0 * nd * S.F + 2.0 * Ed * hF + nd * S.h)}};
+    if (err == hipSuccess) err = bwd_gemms(g, cb, opt, w, s);
     if (err == hipSuccess) {
       KernelTimer kt(MEMFINE_K_UNPERMUTE, s, nd * S.h,
                      es * (nd * S.h + td * S.h) + 4.0 * nd * (g.P + 2));

@@ -159,4 +159,163 @@ hipError_t launch_unpermute(int dtype, const void* dxp, const float* dgp, int P,
   return hipGetLastError();
 }
 
+// ------------------------------------------------ expert-ordered chunks
+// The chunk holds rows [p0, p1) of the layer's grouped rows; every token
+// reads its k row ids and adds the rows that fall in the chunk, in slot
+// order, to an fp32 sum.  The chunk holding the token's first grouped row
+// writes the sum; later chunks add it to the stored value (one rounding to
+// the storage type per chunk).  A token whose slots are all dropped is
+// written as 0 by the first chunk.
+constexpr int kNoRow = 0x7fffffff;
+
+template <typename T, bool kGates>
+__device__ __forceinline__ void sum_rows_in_chunk(const T* __restrict__ rows,
+                                                  const int32_t* __restrict__ row_of_slot,
+                                                  const float* __restrict__ gates, int64_t t,
+                                                  int h, int k, int c, int p0, int p1,
+                                                  float (&acc)[Elem<T>::kVec], bool& any,
+                                                  int& rmin) {
+  constexpr int V = Elem<T>::kVec;
+#pragma unroll
+  for (int q = 0; q < V; ++q) acc[q] = 0.f;
+  any = false;
+  rmin = kNoRow;
+  for (int j0 = 0; j0 < k; j0 += 8) {
+    int r[8];
+    float g[8];
+    u32x4_t v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bool in = j0 + j < k;
+      r[j] = in ? row_of_slot[t * k + j0 + j] : -1;
+      g[j] = kGates && in ? gates[t * k + j0 + j] : 1.f;
+      if (r[j] >= 0) rmin = min(rmin, r[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (r[j] >= p0 && r[j] < p1) v[j] = *(const u32x4_t*)(rows + (int64_t)(r[j] - p0) * h + c * V);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (!(r[j] >= p0 && r[j] < p1)) continue;
+      any = true;
+      float f[V];
+      unpack16(v[j], f, (T*)nullptr);
+#pragma unroll
+      for (int q = 0; q < V; ++q) acc[q] = kGates ? fmaf(g[j], f[q], acc[q]) : acc[q] + f[q];
+    }
+  }
+}
+
+// out[t] = sum (first chunk of the token) or out[t] + sum (later chunks)
+template <typename T>
+__device__ __forceinline__ void store_chunk_sum(T* __restrict__ out, int64_t t, int h, int c,
+                                                float (&acc)[Elem<T>::kVec], bool any, int rmin,
+                                                int p0, int p1) {
+  constexpr int V = Elem<T>::kVec;
+  const bool first = (rmin >= p0 && rmin < p1) || (rmin == kNoRow && p0 == 0);
+  if (!any && !first) return;
+  u32x4_t* o = (u32x4_t*)(out + t * h + c * V);
+  if (!first) {
+    float f[V];
+    unpack16(*o, f, (T*)nullptr);
+#pragma unroll
+    for (int q = 0; q < V; ++q) acc[q] = f[q] + acc[q];
+  }
+  *o = pack16(acc, (T*)nullptr);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void combine_rows_kernel(const T* __restrict__ y,
+                                                           const int32_t* __restrict__ row_of_slot,
+                                                           const float* __restrict__ gates,
+                                                           int64_t tokens, int h, int k, int p0,
+                                                           int p1, T* __restrict__ Y) {
+  constexpr int V = Elem<T>::kVec;
+  const int vpr = h / V;
+  const int64_t gid = blockIdx.x * 256ll + threadIdx.x;
+  if (gid >= tokens * vpr) return;
+  const int64_t t = gid / vpr;
+  const int c = (int)(gid % vpr);
+  float acc[V];
+  bool any;
+  int rmin;
+  sum_rows_in_chunk<T, true>(y, row_of_slot, gates, t, h, k, c, p0, p1, acc, any, rmin);
+  store_chunk_sum<T>(Y, t, h, c, acc, any, rmin, p0, p1);
+}
+
+// dgates of slot j of token t, when its row is in the chunk (or it is dropped
+// and this is the first chunk)
+__device__ __forceinline__ void dgate_in_chunk(const float* __restrict__ dgp, int P, int r,
+                                               int p0, int p1, float* __restrict__ dst) {
+  if (r >= p0 && r < p1) *dst = dgate_of_row(dgp, P, r - p0);
+  else if (r < 0 && p0 == 0) *dst = 0.f;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void unpermute_rows_kernel(
+    const T* __restrict__ dxp, const int32_t* __restrict__ row_of_slot, int64_t tokens, int h,
+    int k, int p0, int p1, T* __restrict__ dX, const float* __restrict__ dgp, int P,
+    float* __restrict__ dgates) {
+  constexpr int V = Elem<T>::kVec;
+  const int vpr = h / V;
+  const int64_t gid = blockIdx.x * 256ll + threadIdx.x;
+  if (gid >= tokens * vpr) return;
+  const int64_t t = gid / vpr;
+  const int c = (int)(gid % vpr);
+  float acc[V];
+  bool any;
+  int rmin;
+  sum_rows_in_chunk<T, false>(dxp, row_of_slot, nullptr, t, h, k, c, p0, p1, acc, any, rmin);
+  store_chunk_sum<T>(dX, t, h, c, acc, any, rmin, p0, p1);
+  if (dgp != nullptr && c < k) dgate_in_chunk(dgp, P, row_of_slot[t * k + c], p0, p1, dgates + t * k + c);
+}
+
+__global__ __launch_bounds__(256) void dgate_rows_kernel(const float* __restrict__ dgp, int P,
+                                                         const int32_t* __restrict__ row_of_slot,
+                                                         int64_t nslots, int p0, int p1,
+                                                         float* __restrict__ dgates) {
+  const int64_t i = blockIdx.x * 256ll + threadIdx.x;
+  if (i >= nslots) return;
+  dgate_in_chunk(dgp, P, row_of_slot[i], p0, p1, dgates + i);
+}
+
+hipError_t launch_combine_rows(int dtype, const void* y, const int32_t* row_of_slot,
+                               const float* gates, int64_t T, int h, int k, int p0, int p1, void* Y,
+                               hipStream_t s) {
+  const int V = dtype == 0 ? 8 : 4;
+  const int64_t work = T * (h / V);
+  if (work == 0) return hipSuccess;
+  const int64_t blocks = (work + 255) / 256;
+  if (dtype == 0)
+    combine_rows_kernel<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t*)y, row_of_slot, gates, T, h,
+                                                       k, p0, p1, (bf16_t*)Y);
+  else
+    combine_rows_kernel<float><<<blocks, 256, 0, s>>>((const float*)y, row_of_slot, gates, T, h, k,
+                                                      p0, p1, (float*)Y);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpermute_rows(int dtype, const void* dxp, const float* dgp, int P,
+                                 const int32_t* row_of_slot, int64_t T, int h, int k, int p0,
+                                 int p1, void* dX, float* dgates, hipStream_t s) {
+  const int V = dtype == 0 ? 8 : 4;
+  const int64_t work = T * (h / V);
+  if (work == 0) return hipSuccess;
+  const int64_t blocks = (work + 255) / 256;
+  const bool fused = k <= h / V;  // every token has a thread per slot
+  const float* dgp_f = fused ? dgp : nullptr;
+  if (dtype == 0)
+    unpermute_rows_kernel<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t*)dxp, row_of_slot, T, h, k,
+                                                         p0, p1, (bf16_t*)dX, dgp_f, P, dgates);
+  else
+    unpermute_rows_kernel<float><<<blocks, 256, 0, s>>>((const float*)dxp, row_of_slot, T, h, k,
+                                                        p0, p1, (float*)dX, dgp_f, P, dgates);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || fused) return err;
+  const int64_t nslots = T * k;
+  dgate_rows_kernel<<<(nslots + 255) / 256, 256, 0, s>>>(dgp, P, row_of_slot, nslots, p0, p1,
+                                                         dgates);
+  return hipGetLastError();
+}
+
 }  // namespace memfine

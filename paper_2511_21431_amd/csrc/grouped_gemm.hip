@@ -556,6 +556,7 @@ struct Tile {
   int n0;     // first output column (FC1: first f)
   int K;      // reduction length
   int r0;     // wgrad: first chunk row of the expert
+  int acc;    // wgrad: the accumulators start from the stored dW (add into it)
 };
 
 // m-tile bound for the row-grouped grid: sum_e ceil(c_e / BM) <= this.
@@ -1171,16 +1172,24 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
   int Ku;
   __host__ __device__ static int M(const GemmArgs& g) { return kFC1 ? 2 * g.F : g.h; }
   __host__ __device__ static int N(const GemmArgs& g) { return kFC1 ? g.h : g.F; }
-  __device__ __forceinline__ static bool acc_on(const GemmArgs& g) {
-    return kAcc < 0 ? g.accumulate != 0 : kAcc == 1;
+  // add into dW for tile t: fixed by the instance (kAcc 0 or 1), else per
+  // expert (g.wmode) or per launch (g.accumulate), set by expert_of
+  __device__ __forceinline__ bool acc_of(const Tile& t) const {
+    return kAcc < 0 ? t.acc != 0 : kAcc == 1;
   }
   static constexpr bool kAccLoads = kAcc != 0;
   __host__ __device__ static int tiles_per_expert(const GemmArgs& g) {
     return ((M(g) + C::BM - 1) / C::BM) * ((N(g) + C::BN - 1) / C::BN);
   }
   static int grid(const GemmArgs& g) { return g.E * tiles_per_expert(g); }
+  // experts with tiles in this launch: with per-expert modes, the first
+  // *g.wexperts of g.order (the others have no rows in the chunk)
+  __device__ __forceinline__ static int tile_experts(const GemmArgs& g) {
+    if constexpr (kAcc >= 0) return g.E;  // (instances without per-expert modes)
+    else return g.wmode != nullptr ? __builtin_amdgcn_readfirstlane(*g.wexperts) : g.E;
+  }
   __device__ __forceinline__ static int total_tiles(const GemmArgs& g) {
-    return g.E * tiles_per_expert(g);
+    return tile_experts(g) * tiles_per_expert(g);
   }
   // does wave (wm, wn) own any element of the tile?
   __device__ __forceinline__ bool active(const GemmArgs& g, const Tile& t, int wm, int wn) const {
@@ -1190,7 +1199,12 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
     t.e = g.order[rank];
     t.r0 = g.offsets[t.e];
     t.K = g.offsets[t.e + 1] - t.r0;
-    return !(t.K == 0 && acc_on(g));  // nothing to add
+    if constexpr (kAcc < 0) {
+      const int m = g.wmode != nullptr ? g.wmode[t.e] : (g.accumulate != 0 ? 2 : 1);
+      if (m == 0) return false;
+      t.acc = m == 2;
+    }
+    return !(t.K == 0 && acc_of(t));  // nothing to add
   }
   // logical tile L: expert rank L / per (experts in descending row count),
   // then the tile of that expert's grid in raster order
@@ -1199,7 +1213,7 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
     const int per = mtn * ntn;
     const int L = logical_of(g.raster, id, n);
     const int rank = L / per;
-    if (rank >= g.E) return false;
+    if (rank >= tile_experts(g)) return false;
     int mt, nt;
     logical_coords(g.raster, L - rank * per, mtn, ntn, mt, nt);
     if (!expert_of(g, t, rank)) return false;
@@ -1214,7 +1228,7 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
     const int mtn2 = (M(g) + 2 * C::BM - 1) / (2 * C::BM), ntn2 = (N(g) + 2 * C::BN - 1) / (2 * C::BN);
     const int per2 = mtn2 * ntn2;
     const int rank = b / per2;
-    if (rank >= g.E) return false;
+    if (rank >= tile_experts(g)) return false;
     int mt, nt;
     logical_coords(g.raster, b - rank * per2, mtn2, ntn2, mt, nt);
     if (!expert_of(g, t, rank)) return false;
@@ -1301,7 +1315,7 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
   // from clamped in-range addresses; those accumulators are never stored.
   __device__ __forceinline__ void init_acc(const GemmArgs& g, const Tile& t, Accum<C>& acc, int wm,
                                           int wn, int lane) const {
-    if (!acc_on(g)) {
+    if (!acc_of(t)) {
       zero_acc(acc);
       return;
     }
@@ -1489,7 +1503,7 @@ __device__ __forceinline__ void run_located(const GemmArgs& g, char* smem, P& p,
   // merges this entry with the loop's own), where they also wait for the
   // copies each K step has just issued.
   if constexpr (AccLoads<P>::value)
-    if (p.acc_on(g)) wait_vm<0>();
+    if (p.acc_of(t)) wait_vm<0>();
   constexpr int kCopies = P::OA::I + P::OB::I;  // copy instructions per wave per K tile
   const int nk = k_tiles<T, C>(t);
   if constexpr (C::DIRECT) {
@@ -1948,9 +1962,11 @@ hipError_t launch_fc2_fwd(const GemmArgs& g, hipStream_t s) { return launch_auto
 hipError_t launch_fc2_dgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<ProbFC2Dgrad>(g, s); }
 hipError_t launch_fc1_dgrad(const GemmArgs& g, hipStream_t s) { return launch_auto<ProbFC1Dgrad>(g, s); }
 hipError_t launch_fc2_wgrad(const GemmArgs& g, hipStream_t s) {
+  if (g.wmode != nullptr) return launch_auto<FC2W>(g, s);  // per-expert modes
   return g.accumulate ? launch_auto<FC2WAdd>(g, s) : launch_auto<FC2WNew>(g, s);
 }
 hipError_t launch_fc1_wgrad(const GemmArgs& g, hipStream_t s) {
+  if (g.wmode != nullptr) return launch_auto<FC1W>(g, s);  // per-expert modes
   return g.accumulate ? launch_auto<FC1WAdd>(g, s) : launch_auto<FC1WNew>(g, s);
 }
 hipError_t launch_fc1_dgrad_wgrad(const GemmArgs& g, hipStream_t s) {

@@ -39,6 +39,17 @@ hipError_t launch_count(const int32_t* idx, int64_t nslots, int E, int32_t* work
 hipError_t launch_dispatch(const int32_t* idx, const float* gates, int64_t slot0, int n, int E,
                            int k, const ChunkMeta& m, hipStream_t s);
 
+// Expert-ordered chunks: chunk c is rows [p0, p1) of the layer's slots
+// grouped by expert (one dispatch over all tokens).  From the layer's
+// offsets [E + 1], the chunk's view: its offsets [E + 1] (rows relative to
+// p0), its experts with a weight-gradient tile first, by descending row
+// count [E], their number [1], and each expert's weight-gradient mode [E]
+// (0: no tile, 1: overwrite dW, 2: add to dW).  `first`: the first chunk
+// (overwrites the dW of experts without rows unless `accumulate`).
+hipError_t launch_chunk_view(const int32_t* offsets, int E, int p0, int p1, int first,
+                             int accumulate, int32_t* offsets_c, int32_t* order_c,
+                             int32_t* wexperts, int32_t* wmode, hipStream_t s);
+
 // Gate-weighted combine, Y[t0 + i] = sum_j g[t, j] * y[row_of_slot[i*k + j]].
 hipError_t launch_combine(int dtype, const void* y, const int32_t* row_of_slot, const float* gates,
                           int64_t t0, int tokens, int h, int k, void* Y, hipStream_t s);
@@ -46,6 +57,18 @@ hipError_t launch_combine(int dtype, const void* y, const int32_t* row_of_slot, 
 hipError_t launch_unpermute(int dtype, const void* dxp, const float* dgp, int P,
                             const int32_t* row_of_slot, int64_t t0, int tokens, int h, int k,
                             void* dX, float* dgates, hipStream_t s);
+
+// The same over all T tokens for an expert-ordered chunk, rows [p0, p1) of
+// the layer's grouped rows (y and dxp hold those rows, from row p0): each
+// token adds its slots in the chunk to Y (dX), and the chunk that holds its
+// first grouped row overwrites instead (the first chunk, for a token whose
+// slots are all dropped).  dgates of the chunk's slots are written.
+hipError_t launch_combine_rows(int dtype, const void* y, const int32_t* row_of_slot,
+                               const float* gates, int64_t T, int h, int k, int p0, int p1, void* Y,
+                               hipStream_t s);
+hipError_t launch_unpermute_rows(int dtype, const void* dxp, const float* dgp, int P,
+                                 const int32_t* row_of_slot, int64_t T, int h, int k, int p0,
+                                 int p1, void* dX, float* dgates, hipStream_t s);
 
 // Grouped GEMMs.  Row-grouped problems: rows [offsets[e], offsets[e+1]) belong
 // to expert e.  n is the chunk's slot count (an upper bound for the grid).
@@ -70,6 +93,8 @@ struct GemmArgs {
   float* dW1;        // [E, 2F, h]
   float* dW2;        // [E, h, F]
   int accumulate;    // wgrad: 1 = add into dW, 0 = overwrite
+  const int32_t* wmode;     // wgrad, or null: per expert 0 no tile, 1 overwrite, 2 add
+  const int32_t* wexperts;  // wgrad with wmode: experts with a tile (the first of order)
   int64_t T_h_bytes; // bytes of X (and of dY): T * h * element size
   int tile_override; // 0: per problem; 1: 128 x 128; 2: 256 x 256 direct; 3: 256 x 256 staged
   int raster;        // tile order: -1 per problem; 0 row-major; 1..3 XCD blocks, groups of 4/8/16 m-tiles; 4 XCD blocks, row-major

@@ -279,4 +279,53 @@ hipError_t launch_dispatch(const int32_t* idx, const float* gates, int64_t slot0
   return hipGetLastError();
 }
 
+// The view of an expert-ordered chunk, rows [p0, p1) of the layer's grouped
+// rows: one thread per expert (E <= 1024).  The experts that get a weight-
+// gradient tile (mode != 0) come first in order_c, by descending row count
+// in the chunk (ties: lower id), then the rest by id.
+__global__ __launch_bounds__(1024) void chunk_view_kernel(
+    const int32_t* __restrict__ offsets, int E, int p0, int p1, int first, int accumulate,
+    int32_t* __restrict__ offsets_c, int32_t* __restrict__ order_c,
+    int32_t* __restrict__ wexperts, int32_t* __restrict__ wmode) {
+  __shared__ int32_t key[1024];
+  __shared__ int32_t n_tiles;
+  const int e = threadIdx.x;
+  if (e == 0) n_tiles = 0;
+  __syncthreads();
+  int k = -1;
+  if (e < E) {
+    const int lo = offsets[e], hi = offsets[e + 1];
+    const int a = min(max(lo, p0), p1), b = min(max(hi, p0), p1);
+    offsets_c[e] = a - p0;
+    if (e == E - 1) offsets_c[E] = b - p0;
+    const int rows = b - a;
+    int m;
+    if (rows > 0) m = (!accumulate && lo >= p0) ? 1 : 2;  // the expert's first rows: overwrite
+    else m = (lo == hi && first && !accumulate) ? 1 : 0;  // no rows at all: zeros, once
+    wmode[e] = m;
+    if (m != 0) atomicAdd(&n_tiles, 1);
+    k = m != 0 ? rows : -1;  // sort key: experts without a tile last
+    key[e] = k;
+  }
+  __syncthreads();
+  if (e < E) {
+    int rank = 0;
+    for (int q = 0; q < E; ++q) {
+      const int kq = key[q];
+      rank += (kq > k) || (kq == k && q < e);
+    }
+    order_c[rank] = e;
+  }
+  if (e == 0) *wexperts = n_tiles;
+}
+
+hipError_t launch_chunk_view(const int32_t* offsets, int E, int p0, int p1, int first,
+                             int accumulate, int32_t* offsets_c, int32_t* order_c,
+                             int32_t* wexperts, int32_t* wmode, hipStream_t s) {
+  if (E < 1 || E > 1024) return hipErrorInvalidValue;
+  chunk_view_kernel<<<1, 1024, 0, s>>>(offsets, E, p0, p1, first, accumulate, offsets_c, order_c,
+                                       wexperts, wmode);
+  return hipGetLastError();
+}
+
 }  // namespace memfine

@@ -49,11 +49,13 @@ def test_launch_options_roundtrip_and_validation():
     L = _lib.lib()
     mf.memfine_set_launch_options()
     assert mf.memfine_get_launch_options() == {"tile": 0, "raster": -1, "split_tail": 1,
-                                               "pair": 0, "streams": 0}
-    mf.memfine_set_launch_options(tile=mf.TILE_256_REG, raster=3, split_tail=False, pair=True)
+                                               "pair": 0, "streams": 0, "chunk_order": 0}
+    mf.memfine_set_launch_options(tile=mf.TILE_256_REG, raster=3, split_tail=False, pair=True,
+                                  chunk_order=mf.CHUNK_EXPERTS)
     assert mf.memfine_get_launch_options() == {"tile": 3, "raster": 3, "split_tail": 0,
-                                               "pair": 1, "streams": 0}
-    for bad in (dict(tile=4), dict(tile=-1), dict(raster=5), dict(raster=-2)):
+                                               "pair": 1, "streams": 0, "chunk_order": 1}
+    for bad in (dict(tile=4), dict(tile=-1), dict(raster=5), dict(raster=-2),
+                dict(chunk_order=2), dict(chunk_order=-1)):
         with pytest.raises(mf.MemfineError):
             mf.memfine_set_launch_options(**bad)
     assert mf.memfine_get_launch_options()["tile"] == 3       # unchanged by the rejected calls
@@ -191,6 +193,38 @@ def test_workspace_bytes(T, h, F, E, k, dtype):
         assert vals[0] >= T * k * per_slot
     # the backward holds more per slot than the forward
     assert mf.memfine_workspace_bytes(s, 1, mf.PASS_BWD) > mf.memfine_workspace_bytes(s, 1, mf.PASS_FWD)
+
+
+def test_workspace_bytes_expert_order():
+    """Expert-ordered chunks: the layer's routing tables for all N = T k slots
+    (16 bytes per slot and more) are held for the whole call, beside one
+    chunk's intermediates for at most ceil(N / C) rows; the planner's
+    workspace check follows the option."""
+    T, h, F, E, k = 8192, 7168, 2048, 32, 8
+    s = mf.make_shape(T, h, F, E, k, mf.BF16)
+    N = T * k
+    tok = {C: mf.memfine_workspace_bytes(s, C, mf.PASS_BWD) for C in (1, 2, 4, 8, 16)}
+    try:
+        mf.memfine_set_launch_options(chunk_order=mf.CHUNK_EXPERTS)
+        ex = {C: mf.memfine_workspace_bytes(s, C, mf.PASS_BWD) for C in (1, 2, 3, 4, 8, 16, T, T + 9)}
+        vals = list(ex.values())
+        assert all(a >= b for a, b in zip(vals, vals[1:])) and ex[T] == ex[T + 9]
+        tables = ex[T]                          # at C = T a chunk holds k rows
+        assert tables >= 16 * N
+        per_row = 2 * (3 * F + h)               # u, g*a and the input gradient, bf16
+        for C in (1, 2, 4, 8, 16):
+            rows = -(-N // C)
+            assert ex[C] - tables >= (rows - k) * per_row
+            # the same intermediates as the token order's chunk, plus the tables
+            assert abs((ex[C] - tables) - (tok[C] - 16 * rows)) < 0.01 * tok[C] + 2 ** 20
+        counts = [N // E] * E
+        for budget in (5e9, 1e10, 2e10, 4e10):
+            rc, C, info = mf.memfine_plan(s, counts, int(budget), bins=(1, 2, 4, 8, 16))
+            assert info["workspace_bytes"] == ex[C]
+            if rc == 0:
+                assert ex[C] <= budget
+    finally:
+        mf.memfine_set_launch_options()
 
 
 def test_workspace_scales_with_chunks():

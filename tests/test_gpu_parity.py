@@ -467,11 +467,20 @@ def test_full_size_workload2_every_output(mf):
 # the chunk counts their planner picks at the benchmark budgets (C = 8 for
 # both), workload 3 at C = 4, workload 4 at its planner C, and the budget
 # sweep's largest chunk count on workload 5's 131072 tokens
-FULL = [(2, 2), (2, 1), (3, 4), (3, 8), (4, 4), (5, 8), (5, 16)]
+FULL = [(2, 2, 0), (2, 1, 0), (3, 4, 0), (3, 8, 0), (4, 4, 0), (5, 8, 0), (5, 16, 0),
+        (4, 4, 1), (5, 8, 1)]   # last field: chunk order (1: expert-ordered chunks)
 
 
-@pytest.mark.parametrize("cfg,C", FULL)
-def test_full_size_sampled(mf, cfg, C):
+@pytest.mark.parametrize("cfg,C,order", FULL)
+def test_full_size_sampled(mf, cfg, C, order):
+    mf.memfine_set_launch_options(chunk_order=order)
+    try:
+        _full_size_sampled(mf, cfg, C)
+    finally:
+        mf.memfine_set_launch_options()
+
+
+def _full_size_sampled(mf, cfg, C):
     t = torch()
     w = W[cfg]
     log(f"full-size cfg{cfg} C={C}: generating inputs")
