@@ -26,6 +26,9 @@ Prints ONE JSON line (rank 0, N = 1 GPU):
   budget_sweep the planner's chunk count per activation budget with the
                measured peak (workload 5: 4-64 GB; the dense-FFN workload 3,
                where the backward holds more per slot than Table 2's rows)
+  chunk_order  the same step with expert-ordered chunks (a variant outside
+               the paper: runs of whole experts per chunk) beside the
+               paper's token-range chunks, on this workload and workload 4
 """
 from __future__ import annotations
 
@@ -76,6 +79,8 @@ def parse():
                     help="skip the router and block measurement")
     ap.add_argument("--no-budget3", action="store_true",
                     help="skip the workload-3 activation-budget sweep")
+    ap.add_argument("--no-order", action="store_true",
+                    help="skip the chunk-order comparison")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target duration of the oracle sample")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -440,6 +445,14 @@ def main():
     # thresholds) for the paper's Model I, beside the counts-based plan
     mact = mact_model_plan(mf, int(sum(mf.memfine_count(shape, idx, work))))
 
+    # ---- expert-ordered chunks beside the paper's token-range chunks
+    chunk_order = None
+    if not args.no_order:
+        chunk_order = {f"workload{cfg}": compare_orders(mf, torch, step, max(3, args.steps // 2),
+                                                        w, peak)}
+        if cfg != 4 and not args.no_sweep:
+            chunk_order["workload4"] = compare_orders_workload(mf, torch, 4, max(3, args.steps // 2))
+
     # ---- the router in front of the layer: its kernels, and the whole block
     router = None
     if not args.no_router and w.k <= 16:
@@ -495,6 +508,7 @@ def main():
         "budget_sweep": budget_sweep,
         "budget_sweep_workload3": budget_sweep3,
         "mact_model_plan": mact,
+        "chunk_order": chunk_order,
         "router": router,
         "cpu_baseline": cpu,
     }
@@ -571,6 +585,68 @@ def sweep_budgets(mf, torch, cfg):
 MODEL_I = dict(b=1, s=4096, h=7168, a=128, h_d=128, k_a=128, e_n=256, g_e=2048, t=1, c=1,
                v=1, p=4, D_t=2, full_recompute=1)
 MODEL_I_GPU = dict(M_gpu=64 * 10**9, alpha=(9, 10), M_sta=43 * 10**9)
+
+
+def compare_orders(mf, torch, step, steps, w, peak):
+    """The step timed in both chunk orders (launch option chunk_order), same
+    inputs and planner: ms/step, tokens/s, and per-GEMM TFLOP/s from one
+    instrumented step of each."""
+    res = {}
+    for name, order in (("tokens", mf.CHUNK_TOKENS), ("experts", mf.CHUNK_EXPERTS)):
+        mf.memfine_set_launch_options(chunk_order=order)
+        try:
+            step()
+            torch.cuda.synchronize()
+            mf.memfine_profile_begin()
+            C, _ = step()
+            torch.cuda.synchronize()
+            prof = mf.memfine_profile_end()
+            a = time.perf_counter()
+            for _ in range(steps):
+                step()
+            torch.cuda.synchronize()
+            el = time.perf_counter() - a
+        finally:
+            mf.memfine_set_launch_options()
+        res[name] = {"chunks": C, "ms_per_step": round(el * 1e3 / steps, 4),
+                     "tokens_per_s": round(w.T * steps / el, 1),
+                     "gemm": gemm_table(prof, peak),
+                     "combine_ms": round(prof.get("combine", {}).get("total_ms", 0.0), 4),
+                     "unpermute_ms": round(prof.get("unpermute", {}).get("total_ms", 0.0), 4)}
+        log(f"[bench] chunk order {name}: C={C}, {res[name]['ms_per_step']:.3f} ms/step, "
+            f"{res[name]['tokens_per_s']:.0f} tokens/s")
+    return res
+
+
+def compare_orders_workload(mf, torch, cfg, steps):
+    """compare_orders on workload `cfg` with its own inputs and budget."""
+    import moe_workloads as mw
+    w = mw.WORKLOADS[cfg]
+    log(f"[bench] chunk order, workload {cfg} {w.name}: generating inputs")
+    shape = mf.make_shape(w.T, w.h, w.F, w.E, w.k, mf.BF16)
+    idx_np, gates_np = mw.make_routing(w, cfg)
+    dev = mw.make_tensors_device(w, cfg, "cuda")
+    idx = torch.from_numpy(idx_np).cuda()
+    gates = torch.from_numpy(gates_np).cuda()
+    Y = torch.empty((w.T, w.h), dtype=torch.bfloat16, device="cuda")
+    dX = torch.empty_like(Y)
+    dW1 = torch.empty((w.E, 2 * w.F, w.h), dtype=torch.float32, device="cuda")
+    dW2 = torch.empty((w.E, w.h, w.F), dtype=torch.float32, device="cuda")
+    dg = torch.empty((w.T, w.k), dtype=torch.float32, device="cuda")
+    work = torch.zeros(w.E + 1, dtype=torch.int32, device="cuda")
+
+    def step():
+        counts = mf.memfine_count(shape, idx, work)
+        rc, C, info = mf.memfine_plan(shape, counts, DEFAULT_BUDGET[cfg], bins=w.bins)
+        mf.memfine_moe_fwd(shape, C, dev["X"], idx, gates, dev["W1"], dev["W2"], Y)
+        mf.memfine_moe_bwd(shape, C, dev["X"], idx, gates, dev["W1"], dev["W2"], dev["dY"], dX,
+                           dW1, dW2, dg)
+        return C, info
+
+    res = compare_orders(mf, torch, step, steps, w, PEAK_TFLOPS[w.dtype])
+    del dev, Y, dX, dW1, dW2
+    torch.cuda.empty_cache()
+    return res
 
 
 def mact_model_plan(mf, s_recv):

@@ -377,7 +377,11 @@ int memfine_moe_bwd(const memfine_shape* shape, int32_t chunks, const void* d_X,
  *   d_idx     int32 [T, k] out, largest logit first
  *   d_gates   float [T, k] out
  *   d_logits  float [T, E] out, may be NULL
- * Asynchronous; no working memory.
+ * Asynchronous.  Up to 64 logits (or E not a multiple of 32) one fused
+ * kernel, no working memory; wider routers compute the logits as a grouped
+ * GEMM and select from them, taking 256 bytes and, when d_logits is NULL,
+ * the [T, E] fp32 logits from the library's per-stream workspace (as a
+ * layer call with a NULL allocator does); MEMFINE_ERR_OOM if that fails.
  */
 int memfine_router_fwd(const memfine_shape* shape, const void* d_X, const void* d_Wr,
                        int32_t* d_idx, float* d_gates, float* d_logits, void* stream);

@@ -1178,8 +1178,42 @@ int memfine_router_fwd(const memfine_shape* shape, const void* d_X, const void* 
   KernelTimer kt(MEMFINE_K_ROUTER_FWD, s, 2.0 * Td * S.h * S.E,
                  es * (Td * S.h + (double)S.E * S.h) + 8.0 * Td * S.k +
                      (d_logits ? 4.0 * Td * S.E : 0.0));
-  return hip_status(launch_router_fwd(S.dtype, d_X, d_Wr, S.T, S.h, S.E, S.k, d_idx, d_gates,
-                                      d_logits, s));
+  if (S.E <= 64 || S.E % 32 != 0)
+    return hip_status(launch_router_fwd(S.dtype, d_X, d_Wr, S.T, S.h, S.E, S.k, d_idx, d_gates,
+                                        d_logits, s));
+  // Wide routers: the logits as a grouped GEMM on 256-token tiles (each tile
+  // reads Wr once; one fused kernel per 32 tokens read it T / 32 times), then
+  // their top-k.  Working memory: the {0, T} row offsets of the GEMM's one
+  // "expert" and, without d_logits, the logits themselves.
+  const int64_t off_bytes = 256, lg_bytes = d_logits ? 0 : S.T * (int64_t)S.E * 4;
+  void* ws = ws_alloc(nullptr, (size_t)(off_bytes + lg_bytes), s);
+  if (!ws) return MEMFINE_ERR_OOM;
+  int32_t* off = (int32_t*)ws;
+  float* lg = d_logits ? d_logits : (float*)((char*)ws + off_bytes);
+  hipError_t err = launch_fill_i32(off, 1, 0, s);
+  if (err == hipSuccess) err = launch_fill_i32(off + 1, 1, (int32_t)S.T, s);
+  if (err == hipSuccess) {
+    const memfine_launch_options opt = launch_options();
+    GemmArgs g = {};
+    g.dtype = S.dtype;
+    g.n = (int)S.T;
+    g.E = 1;
+    g.h = S.E;   // output columns: the logits
+    g.F = S.h;   // reduction: the hidden size
+    g.offsets = off;
+    g.a = const_cast<void*>(d_X);
+    g.W2 = d_Wr;
+    g.y = lg;
+    g.T_h_bytes = S.T * (int64_t)S.h * elem_bytes(S);
+    g.tile_override = opt.tile;
+    g.raster = opt.raster;
+    g.cus = device_cus();
+    g.split_tail = opt.split_tail;
+    err = launch_router_logits(g, s);
+  }
+  if (err == hipSuccess) err = launch_router_topk(lg, S.T, S.E, S.k, d_idx, d_gates, s);
+  ws_release(nullptr, ws, (size_t)(off_bytes + lg_bytes), s);
+  return hip_status(err);
 }
 
 int memfine_router_bwd(const memfine_shape* shape, const void* d_X, const void* d_Wr,

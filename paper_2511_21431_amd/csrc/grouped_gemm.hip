@@ -1019,6 +1019,16 @@ template <typename T, class C> struct ProbFC2 {
   }
 };
 
+// Router logits: logits[t, e] = sum_k X[t, k] Wr[e, k], stored in fp32.
+// FC2's problem with one "expert" holding all T rows: X in `a` (K = h in
+// GemmArgs.F), Wr in `W2` (its E_r rows in GemmArgs.h), the logits in `y`.
+template <typename T, class C> struct ProbLogits : ProbFC2<T, C> {
+  __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
+                                           int wm, int wn, int lane, char*) const {
+    store_rows<float, C>(acc, (float*)g.y, g.h, t, wm, wn, lane, nullptr);
+  }
+};
+
 // Backward FC2 dgrad: dA[m, f] = sum_o dY[tok(m), o] W2[e, o, f]     K = h
 // (written to `ag`; the SwiGLU backward happens in the FC1 recomputation).
 template <typename T, class C> struct ProbFC2Dgrad {
@@ -1968,6 +1978,9 @@ hipError_t launch_fc2_wgrad(const GemmArgs& g, hipStream_t s) {
 hipError_t launch_fc1_wgrad(const GemmArgs& g, hipStream_t s) {
   if (g.wmode != nullptr) return launch_auto<FC1W>(g, s);  // per-expert modes
   return g.accumulate ? launch_auto<FC1WAdd>(g, s) : launch_auto<FC1WNew>(g, s);
+}
+hipError_t launch_router_logits(const GemmArgs& g, hipStream_t s) {
+  return launch_auto<ProbLogits>(g, s);
 }
 hipError_t launch_fc1_dgrad_wgrad(const GemmArgs& g, hipStream_t s) {
   return launch_pair<ProbFC1Dgrad, FC1W>(g, s);

@@ -110,6 +110,13 @@ int dgate_partials(int F);
 // top-k and renormalised gates; logits may be null.
 hipError_t launch_router_fwd(int dtype, const void* X, const void* Wr, int64_t T, int h, int E,
                              int k, int32_t* idx, float* gates, float* logits, hipStream_t s);
+// Router forward in two steps for wide routers: the logits [T, E] (fp32) as a
+// grouped GEMM (launch_router_logits: one "expert" of T rows; X in a, K = h
+// in F, Wr in W2, E in h, logits in y, offsets {0, T}), then their top-k
+// (64 < E <= 256, k <= 16) with the selection and gates of launch_router_fwd.
+hipError_t launch_router_logits(const GemmArgs& g, hipStream_t s);
+hipError_t launch_router_topk(const float* logits, int64_t T, int E, int k, int32_t* idx,
+                              float* gates, hipStream_t s);
 // Router backward, per token: dX (+)= dz Wr and the dense dz rows D [T, EP].
 hipError_t launch_router_bwd_dx(int dtype, const void* Wr, const int32_t* idx, const float* gates,
                                 const float* dgates, int64_t T, int h, int E, int k, int EP,

@@ -180,6 +180,62 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_fwd_kernel(
   }
 }
 
+// Top-k of one token whose logits a wave holds (lane l: experts l + 64 q,
+// q < V; entries of experts >= E are ignored): k rounds of a wave-wide
+// arg-max over (logit, lower id) by shuffles, so the selection and its
+// order are those of the narrow kernel; then lanes 0..k-1 write the
+// selected ids, largest first, and the gates renormalised over them (the
+// full softmax's denominator cancels).
+template <int V>
+__device__ __forceinline__ void wave_topk(const float (&v)[V], int E, int k, int lane, int64_t t,
+                                          int32_t* __restrict__ idx, float* __restrict__ gates) {
+  uint32_t taken = 0;
+  float selv[16];
+  int seli[16];
+  for (int j = 0; j < k; ++j) {
+    float bv = -INFINITY;
+    int bi = INT32_MAX;
+#pragma unroll
+    for (int q = 0; q < V; ++q) {
+      const int e = lane + 64 * q;
+      if (e < E && !((taken >> q) & 1u) && (v[q] > bv || (v[q] == bv && e < bi))) {
+        bv = v[q];
+        bi = e;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (ov > bv || (ov == bv && oi < bi)) {
+        bv = ov;
+        bi = oi;
+      }
+    }
+    if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj)
+      if (jj == j) {
+        selv[jj] = bv;
+        seli[jj] = bi;
+      }
+  }
+  // renormalised softmax over the selected logits; selv[0] is the largest
+  float e[16], sum = 0.f;
+#pragma unroll
+  for (int jj = 0; jj < 16; ++jj) {
+    e[jj] = jj < k ? __expf(selv[jj] - selv[0]) : 0.f;
+    sum += e[jj];
+  }
+  const float inv = 1.f / sum;
+#pragma unroll
+  for (int jj = 0; jj < 16; ++jj)
+    if (jj < k && lane == jj) {
+      idx[t * k + jj] = seli[jj];
+      gates[t * k + jj] = e[jj] * inv;
+    }
+}
+
 // Forward for wide routers (64 < E <= 256 logits per token, the width of a
 // 256-expert model).  A workgroup owns 32 tokens; wave w multiplies them
 // with expert blocks w NBW .. w NBW + NBW - 1 (32 experts each) over the
@@ -254,52 +310,28 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_fwd_wide_kernel(
       v[j] = lg[tok][e];
       if (logits && e < E) logits[t * E + e] = v[j];
     }
-    uint32_t taken = 0;
-    float selv[16];
-    int seli[16];
-    for (int j = 0; j < k; ++j) {
-      float bv = -INFINITY;
-      int bi = INT32_MAX;
-#pragma unroll
-      for (int q = 0; q < V; ++q) {
-        const int e = lane + 64 * q;
-        if (e < E && !((taken >> q) & 1u) && (v[q] > bv || (v[q] == bv && e < bi))) {
-          bv = v[q];
-          bi = e;
-        }
-      }
-#pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) {
-        const float ov = __shfl_xor(bv, o, 64);
-        const int oi = __shfl_xor(bi, o, 64);
-        if (ov > bv || (ov == bv && oi < bi)) {
-          bv = ov;
-          bi = oi;
-        }
-      }
-      if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
-#pragma unroll
-      for (int jj = 0; jj < 16; ++jj)
-        if (jj == j) {
-          selv[jj] = bv;
-          seli[jj] = bi;
-        }
-    }
-    // renormalised softmax over the selected logits; selv[0] is the largest
-    float e[16], sum = 0.f;
-#pragma unroll
-    for (int jj = 0; jj < 16; ++jj) {
-      e[jj] = jj < k ? __expf(selv[jj] - selv[0]) : 0.f;
-      sum += e[jj];
-    }
-    const float inv = 1.f / sum;
-#pragma unroll
-    for (int jj = 0; jj < 16; ++jj)
-      if (jj < k && lane == jj) {
-        idx[t * k + jj] = seli[jj];
-        gates[t * k + jj] = e[jj] * inv;
-      }
+    wave_topk<V>(v, E, k, lane, t, idx, gates);
   }
+}
+
+// Top-k of logits already in memory (fp32 [T, E], 64 < E <= 256), one wave
+// per token, with the selection and gates of the kernels above: the router's
+// second step when the logits come from the grouped GEMM.
+__global__ __launch_bounds__(256) void router_topk_kernel(const float* __restrict__ logits,
+                                                          int64_t T_, int E, int k,
+                                                          int32_t* __restrict__ idx,
+                                                          float* __restrict__ gates) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T_) return;  // uniform over the wave
+  constexpr int V = 4;
+  float v[V];
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const int e = lane + 64 * j;
+    v[j] = e < E ? logits[t * E + e] : 0.f;
+  }
+  wave_topk<V>(v, E, k, lane, t, idx, gates);
 }
 
 // Backward, one wave per token (grid-stride): dz_j = g_j (dg_j - sum g dg);
@@ -453,6 +485,14 @@ hipError_t launch_router_fwd(int dtype, const void* X, const void* Wr, int64_t T
     else
       router_fwd_wide_kernel<float, 2><<<grid, block, 0, s>>>(x, wr, T, h, E, k, idx, gates, logits);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_router_topk(const float* logits, int64_t T, int E, int k, int32_t* idx,
+                              float* gates, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (E > 256 || k > 16) return hipErrorInvalidValue;
+  router_topk_kernel<<<(unsigned)((T + 3) / 4), 256, 0, s>>>(logits, T, E, k, idx, gates);
   return hipGetLastError();
 }
 

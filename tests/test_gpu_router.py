@@ -74,14 +74,18 @@ def run_router(mf, w, X, Wr, dg, accumulate_dX=None):
             "dX": host(dX), "dWr": host(dWr)}
 
 
-# (T, h, E, k, dtype): narrow routers (E <= 64), wide ones (64 < E <= 256),
-# and the router of the paper's Table 3 models at one GPU's token count
-# (T = 8192, h = 7168, 256 routed experts, top-8)
+# (T, h, E, k, dtype): narrow routers (E <= 64, one fused kernel), wide ones
+# (64 < E <= 256: a fused kernel, or, for E a multiple of 32, the logits as a
+# grouped GEMM and a top-k kernel), and the router of the paper's Table 3
+# models at one GPU's token count (T = 8192, h = 7168, 256 routed experts,
+# top-8)
 CASES = [(1000, 512, 16, 4, "bf16"), (777, 256, 6, 2, "bf16"), (513, 128, 33, 8, "bf16"),
          (256, 64, 64, 16, "bf16"), (300, 192, 4, 4, "bf16"), (200, 128, 5, 1, "bf16"),
          (1000, 512, 16, 4, "f32"), (129, 64, 40, 3, "f32"),
          (700, 256, 100, 6, "bf16"), (513, 128, 256, 8, "bf16"), (333, 64, 65, 16, "bf16"),
-         (300, 64, 129, 16, "f32"), (1000, 512, 200, 4, "f32"), (8192, 7168, 256, 8, "bf16")]
+         (300, 64, 129, 16, "f32"), (1000, 512, 200, 4, "f32"), (8192, 7168, 256, 8, "bf16"),
+         (600, 256, 96, 5, "bf16"), (700, 128, 160, 4, "f32"), (2048, 1024, 128, 8, "bf16"),
+         (4099, 512, 224, 16, "bf16")]
 
 
 def check_against_fp64_logits(mf, w, X, Wr, dg, got, tol):
@@ -156,6 +160,24 @@ def test_router_ties_take_the_lower_id(mf):
         assert np.array_equal(got["logits"][:, 1::2], got["logits"][:, 0::2])
         assert np.array_equal(got["idx"], own["idx"])
         assert np.all(got["idx"][:, 0] % 2 == 0)   # of each tied pair, the even id first
+
+
+@pytest.mark.parametrize("E", [96, 256])
+def test_router_without_logits_output(mf, E):
+    """Without a logits output the wide router keeps its logits in working
+    memory: the same ids and gates, bit for bit, as with the output."""
+    t = torch()
+    w, X, Wr, dg = make(1500, 256, E, 8, "bf16", seed=E + 3)
+    Xd, Wd = dev(X, "bf16"), dev(Wr, "bf16")
+    out = []
+    for with_logits in (True, False):
+        idx = t.full((w.T, w.k), -1, dtype=t.int32, device="cuda")
+        gates = t.full((w.T, w.k), float("nan"), device="cuda")
+        logits = t.empty((w.T, w.E), device="cuda") if with_logits else None
+        mf.memfine_router_fwd(shape_of(w), Xd, Wd, idx, gates, logits)
+        t.cuda.synchronize()
+        out.append((idx.cpu().numpy(), host(gates)))
+    assert np.array_equal(out[0][0], out[1][0]) and np.array_equal(out[0][1], out[1][1])
 
 
 def test_router_accumulates_into_dX(mf):
