@@ -1238,10 +1238,15 @@ int memfine_router_bwd(const memfine_shape* shape, const void* d_X, const void* 
   const int ntn = (S.h + 255) / 256;
   const int64_t want = (256 + ntn - 1) / ntn, most = std::max<int64_t>(1, T / 256);
   const int splits = (int)std::max<int64_t>(1, std::min(want, most));
+  // dX (+)= dz Wr: per token in the dz kernel, or (E % 64 == 0, so that the
+  // dense dz rows are whole K tiles) as a grouped GEMM from D, which reads
+  // Wr once per 256-token tile instead of k rows of it per token
+  const bool gemm_dx = S.E % 64 == 0;
   const int64_t o_meta = align256(T * EP * es);
   const int64_t o_order = o_meta + align256((splits + 1) * 4);
   const int64_t o_tok = o_order + align256(splits * 4);
-  const int64_t o_part = o_tok + align256(T * 4);
+  const int64_t o_off1 = o_tok + align256(T * 4);
+  const int64_t o_part = o_off1 + 256;
   const int64_t total = o_part + align256((int64_t)splits * EP * S.h * 4);
   char* ws = (char*)ws_alloc(alloc, (size_t)total, s);
   if (!ws) return MEMFINE_ERR_OOM;
@@ -1249,16 +1254,43 @@ int memfine_router_bwd(const memfine_shape* shape, const void* d_X, const void* 
   int32_t* offsets = (int32_t*)(ws + o_meta);
   int32_t* order = (int32_t*)(ws + o_order);
   int32_t* tok = (int32_t*)(ws + o_tok);
+  int32_t* off1 = (int32_t*)(ws + o_off1);
   float* part = (float*)(ws + o_part);
   const double Td = (double)T, hd = (double)S.h;
-  hipError_t err;
-  {
-    KernelTimer kt(MEMFINE_K_ROUTER_BWD_DX, s, 2.0 * Td * S.k * hd,
-                   (double)es * (Td * hd * (accumulate_dX ? 2.0 : 1.0) + Td * EP) + 12.0 * Td * S.k);
+  hipError_t err = launch_router_split_meta(offsets, order, tok, T, splits, s);
+  if (err == hipSuccess) {
+    KernelTimer kt(MEMFINE_K_ROUTER_BWD_DX, s, 2.0 * Td * (gemm_dx ? EP : S.k) * hd,
+                   (double)es * (Td * hd * (accumulate_dX ? 2.0 : 1.0) +
+                                 Td * EP * (gemm_dx ? 2.0 : 1.0) + (double)S.E * hd) +
+                       12.0 * Td * S.k);
     err = launch_router_bwd_dx(S.dtype, d_Wr, d_idx, d_gates, d_dgates, T, S.h, S.E, S.k,
-                               EP, accumulate_dX, d_dX, D, s);
+                               EP, accumulate_dX, gemm_dx ? 0 : 1, d_dX, D, s);
+    if (err == hipSuccess && gemm_dx) {
+      err = launch_fill_i32(off1, 1, 0, s);
+      if (err == hipSuccess) err = launch_fill_i32(off1 + 1, 1, (int32_t)T, s);
+      if (err == hipSuccess) {
+        const memfine_launch_options opt = launch_options();
+        GemmArgs g = {};
+        g.dtype = S.dtype;
+        g.n = (int)T;
+        g.E = 1;
+        g.h = EP;    // reduction: the dense dz row
+        g.F = S.h;   // output columns: the hidden size
+        g.offsets = off1;
+        g.tok_of_row = tok;   // the identity
+        g.dY = D;
+        g.W2 = d_Wr;
+        g.ag = d_dX;
+        g.accumulate = accumulate_dX;
+        g.T_h_bytes = T * (int64_t)EP * es;
+        g.tile_override = opt.tile;
+        g.raster = opt.raster;
+        g.cus = device_cus();
+        g.split_tail = opt.split_tail;
+        err = launch_router_dx(g, s);
+      }
+    }
   }
-  if (err == hipSuccess) err = launch_router_split_meta(offsets, order, tok, T, splits, s);
   if (err == hipSuccess) {
     // dWr partials: the grouped weight-gradient GEMM over `splits` row ranges
     // of dz^T X (M = EP rows of the dense dz, N = h, K = the range)

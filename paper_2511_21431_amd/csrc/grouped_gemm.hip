@@ -1092,6 +1092,94 @@ template <typename T, class C> struct ProbFC2Dgrad {
   }
 };
 
+// Router backward's input gradient: dX[t, n] (+)= sum_e D[t, e] Wr[e, n],
+// with D the dense dz rows [T, E] (E % 64 == 0).  FC2 dgrad's problem with
+// one "expert" of T rows: D in `dY` (K = E in GemmArgs.h, rows through the
+// identity `tok_of_row`), Wr in `W2` (h columns in GemmArgs.F), dX in `ag`,
+// overwritten or, with `accumulate`, added to in fp32.
+template <typename T, class C> struct ProbRouterDx : ProbFC2Dgrad<T, C> {
+  // reads dX when accumulating; the epilogue then has kStageSlabBytes of the
+  // (idle) stages per wave
+  static constexpr bool kEpilogueLoads = true;
+  __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
+                                           int wm, int wn, int lane, char* slab) const {
+    if (!g.accumulate) {
+      store_rows<T, C>(acc, (T*)g.ag, g.F, t, wm, wn, lane, slab);
+      return;
+    }
+    const int ld = g.F;  // % 64 == 0
+    if constexpr (sizeof(T) == 2 && C::WTN % 64 == 0 && C::NW * kStageSlabBytes <= C::kLds) {
+      // Per 32 rows x 64 columns of the wave's block: the fp32 sums go to the
+      // slab (32 rows of 256 bytes, 16-byte units XOR-swizzled by row), then
+      // each lane takes 8 consecutive columns of one row, adds the stored
+      // bf16 values and writes 16 bytes back: 8 lanes cover one row's 128
+      // contiguous bytes.
+      const int m0 = __builtin_amdgcn_readfirstlane(t.m0);
+      const int mrows = __builtin_amdgcn_readfirstlane(t.mrows);
+      const int n0 = __builtin_amdgcn_readfirstlane(t.n0);
+      const int rr = lane & 31, half = lane >> 5;
+      constexpr int CG = C::WTN / 64;
+#pragma clang loop unroll(full)
+      for (int mb = 0; mb < C::MB; ++mb)
+#pragma clang loop unroll(full)
+        for (int cg = 0; cg < CG; ++cg) {
+#pragma clang loop unroll(full)
+          for (int b = 0; b < 2; ++b)
+#pragma clang loop unroll(full)
+            for (int gq = 0; gq < 4; ++gq) {
+              float v[4];
+              acc_run(acc.v[mb][cg * 2 + b], gq, v);
+              const int unit = b * 8 + gq * 2 + half;  // 4 fp32 columns
+              *(f32x4_t*)(slab + rr * 256 + ((unit ^ (rr & 15)) << 4)) =
+                  (f32x4_t){v[0], v[1], v[2], v[3]};
+            }
+          asm volatile("" ::: "memory");  // the writes above before the reads below
+          const int u8 = lane & 7;         // 8-column group of the row
+#pragma clang loop unroll(full)
+          for (int q = 0; q < 4; ++q) {
+            const int r = (lane >> 3) + 8 * q;
+            const f32x4_t lo = *(const f32x4_t*)(slab + r * 256 + (((2 * u8) ^ (r & 15)) << 4));
+            const f32x4_t hi = *(const f32x4_t*)(slab + r * 256 + (((2 * u8 + 1) ^ (r & 15)) << 4));
+            const int row = wm * C::WTM + mb * 32 + r;
+            const int col = n0 + wn * C::WTN + cg * 64 + u8 * 8;
+            if (row < mrows && col < ld) {
+              u32x4_t* o = (u32x4_t*)((T*)g.ag + (int64_t)(m0 + row) * ld + col);
+              float f[8];
+              unpack16(*o, f, (T*)nullptr);
+#pragma clang loop unroll(full)
+              for (int c = 0; c < 4; ++c) {
+                f[c] += lo[c];
+                f[4 + c] += hi[c];
+              }
+              *o = pack16(f, (T*)nullptr);
+            }
+          }
+          asm volatile("" ::: "memory");  // the reads above before the next writes
+        }
+      return;
+    }
+#pragma clang loop unroll(full)
+    for (int mb = 0; mb < C::MB; ++mb) {
+      const int r = acc_row<C>(wm, mb, lane);
+      if (r >= t.mrows) continue;
+      T* o = (T*)g.ag + (int64_t)(t.m0 + r) * ld;
+#pragma clang loop unroll(full)
+      for (int nb = 0; nb < C::NB; ++nb)
+#pragma clang loop unroll(full)
+        for (int gq = 0; gq < 4; ++gq) {
+          const int n = t.n0 + acc_col<C>(wn, nb, gq, lane);
+          if (n >= ld) continue;
+          float v[4], old[4];
+          acc_run(acc.v[mb][nb], gq, v);
+          Vec4<T>::unpack(Vec4<T>::load_raw(o + n), old);
+#pragma clang loop unroll(full)
+          for (int c = 0; c < 4; ++c) v[c] = old[c] + v[c];
+          Vec4<T>::store(o + n, v);
+        }
+    }
+  }
+};
+
 // Backward FC1 dgrad: dxp[m, n] = sum_c du[m, c] W1[e, c, n].    K = 2F
 template <typename T, class C> struct ProbFC1Dgrad {
   typedef ProbFC1Dgrad ProbSelf;
@@ -1925,6 +2013,9 @@ template <> struct StagedCopies<ProbFC2Dgrad> {
 template <> struct StagedCopies<ProbFC1Dgrad> {
   static constexpr bool value = true;
 };
+template <> struct StagedCopies<ProbRouterDx> {
+  static constexpr bool value = true;
+};
 
 // Pick the tile shape.  The 256 x 256 tile on 8 waves (one workgroup per CU,
 // two waves per SIMD, 128 x 64 per wave) measured fastest on every workload
@@ -1978,6 +2069,9 @@ hipError_t launch_fc2_wgrad(const GemmArgs& g, hipStream_t s) {
 hipError_t launch_fc1_wgrad(const GemmArgs& g, hipStream_t s) {
   if (g.wmode != nullptr) return launch_auto<FC1W>(g, s);  // per-expert modes
   return g.accumulate ? launch_auto<FC1WAdd>(g, s) : launch_auto<FC1WNew>(g, s);
+}
+hipError_t launch_router_dx(const GemmArgs& g, hipStream_t s) {
+  return launch_auto<ProbRouterDx>(g, s);
 }
 hipError_t launch_router_logits(const GemmArgs& g, hipStream_t s) {
   return launch_auto<ProbLogits>(g, s);

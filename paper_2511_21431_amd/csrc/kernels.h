@@ -117,10 +117,15 @@ hipError_t launch_router_fwd(int dtype, const void* X, const void* Wr, int64_t T
 hipError_t launch_router_logits(const GemmArgs& g, hipStream_t s);
 hipError_t launch_router_topk(const float* logits, int64_t T, int E, int k, int32_t* idx,
                               float* gates, hipStream_t s);
-// Router backward, per token: dX (+)= dz Wr and the dense dz rows D [T, EP].
+// Router backward, per token: the dense dz rows D [T, EP] and, with
+// `with_dx`, dX (+)= dz Wr (else launch_router_dx computes it from D).
 hipError_t launch_router_bwd_dx(int dtype, const void* Wr, const int32_t* idx, const float* gates,
                                 const float* dgates, int64_t T, int h, int E, int k, int EP,
-                                int accumulate, void* dX, void* D, hipStream_t s);
+                                int accumulate, int with_dx, void* dX, void* D, hipStream_t s);
+// dX (+)= D Wr as a grouped GEMM (E % 64 == 0): one "expert" of T rows; D in
+// dY (K = E in h, identity tok_of_row), Wr in W2, the hidden size in F, dX in
+// ag, `accumulate` adds to it.
+hipError_t launch_router_dx(const GemmArgs& g, hipStream_t s);
 // Row ranges of S splits of T rows (offsets [S + 1], order [S]) and the
 // identity row -> token table [T], for the split-K weight gradient.
 hipError_t launch_router_split_meta(int32_t* offsets, int32_t* order, int32_t* tok, int64_t T, int S,

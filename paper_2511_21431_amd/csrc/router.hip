@@ -344,7 +344,7 @@ template <typename T>
 __global__ __launch_bounds__(256) void router_bwd_dx_kernel(
     const T* __restrict__ Wr, const int32_t* __restrict__ idx, const float* __restrict__ gates,
     const float* __restrict__ dgates, int64_t T_, int h, int E, int k, int EP, int accumulate,
-    T* __restrict__ dX, T* __restrict__ D) {
+    int with_dx, T* __restrict__ dX, T* __restrict__ D) {
   constexpr int V = Elem<T>::kVec;  // elements per 16-byte vector
   constexpr int NV = 4;             // vectors per lane per pass
   const int lane = threadIdx.x & 63;
@@ -369,7 +369,7 @@ __global__ __launch_bounds__(256) void router_bwd_dx_kernel(
       dzs[j] = __shfl(dz, j, 64);
       ids[j] = j < k ? __shfl(id, j, 64) : -1;
     }
-    for (int c0 = lane * V; c0 < h; c0 += 64 * V * NV) {
+    for (int c0 = lane * V; with_dx && c0 < h; c0 += 64 * V * NV) {
       float acc[NV][V];
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
@@ -498,14 +498,14 @@ hipError_t launch_router_topk(const float* logits, int64_t T, int E, int k, int3
 
 hipError_t launch_router_bwd_dx(int dtype, const void* Wr, const int32_t* idx, const float* gates,
                                 const float* dgates, int64_t T, int h, int E, int k, int EP,
-                                int accumulate, void* dX, void* D, hipStream_t s) {
+                                int accumulate, int with_dx, void* dX, void* D, hipStream_t s) {
   if (T == 0) return hipSuccess;
   const int64_t want = (T + 3) / 4;
   const int blocks = (int)(want < 8192 ? want : 8192);
   if (dtype == 0)
-    router_bwd_dx_kernel<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t*)Wr, idx, gates, dgates, T, h, E, k, EP, accumulate, (bf16_t*)dX, (bf16_t*)D);
+    router_bwd_dx_kernel<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t*)Wr, idx, gates, dgates, T, h, E, k, EP, accumulate, with_dx, (bf16_t*)dX, (bf16_t*)D);
   else
-    router_bwd_dx_kernel<float><<<blocks, 256, 0, s>>>((const float*)Wr, idx, gates, dgates, T, h, E, k, EP, accumulate, (float*)dX, (float*)D);
+    router_bwd_dx_kernel<float><<<blocks, 256, 0, s>>>((const float*)Wr, idx, gates, dgates, T, h, E, k, EP, accumulate, with_dx, (float*)dX, (float*)D);
   return hipGetLastError();
 }
 
