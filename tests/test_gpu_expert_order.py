@@ -170,3 +170,28 @@ def test_expert_order_allocator_peak(mf, experts_order):
         assert alloc.live == {} and alloc.live_bytes == 0
         assert alloc.high_water == pred, (C, alloc.high_water, pred)
         assert pred <= peak <= pred + (4 << 20), (C, peak, pred)
+
+
+def test_expert_order_launch_options_bitwise(mf):
+    """Expert-ordered chunks under the other launch options (paired FC1
+    backward launch, side streams, 128 x 128 tiles): the same results, bit
+    for bit (each output element keeps its order of fp32 sums)."""
+    w, case = case_of("cfg4-like")
+    dev = device_case(w, case)
+    res = {}
+    try:
+        for name, kw in (("default", {}), ("pair", dict(pair=True)), ("streams", dict(streams=True)),
+                         ("tile128", dict(tile=mf.TILE_128))):
+            mf.memfine_set_launch_options(chunk_order=mf.CHUNK_EXPERTS, **kw)
+            log(f"expert order, launch options {name}")
+            Y = host(run_fwd(w, dev, 3))
+            B = {k: host(v) for k, v in run_bwd(w, dev, 3).items()}
+            res[name] = (Y, B)
+    finally:
+        mf.memfine_set_launch_options()
+    Y0, B0 = res["default"]
+    for name, (Y, B) in res.items():
+        assert np.array_equal(Y, Y0), name
+        for key in B0:
+            assert np.array_equal(B[key], B0[key]), (name, key)
+
