@@ -180,10 +180,50 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_fwd_kernel(
   }
 }
 
+// Lane j's value, in a scalar register (uniform).
+__device__ __forceinline__ float lane_value(float v, int j) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), j));
+}
+// One step of a (value, lower index) arg-max with the lane that DPP control
+// `kCtrl` names (a permutation inside each row of 16 lanes).
+template <int kCtrl>
+__device__ __forceinline__ void argmax_dpp(float& v, int& i) {
+  const float ov = __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), kCtrl, 0xf, 0xf, false));
+  const int oi = __builtin_amdgcn_update_dpp(0, i, kCtrl, 0xf, 0xf, false);
+  if (ov > v || (ov == v && oi < i)) {
+    v = ov;
+    i = oi;
+  }
+}
+// The wave's arg-max over (value, lower index), left in every lane: inside
+// each row of 16 lanes by DPP (swap neighbours, swap pairs, mirror halves of
+// 8, mirror the row: after each step a lane holds the best of 2, 4, 8, 16
+// lanes), then the four rows' results through scalar registers.
+__device__ __forceinline__ void wave_argmax(float& v, int& i) {
+  argmax_dpp<0xb1>(v, i);   // quad_perm [1, 0, 3, 2]
+  argmax_dpp<0x4e>(v, i);   // quad_perm [2, 3, 0, 1]
+  argmax_dpp<0x141>(v, i);  // row_half_mirror
+  argmax_dpp<0x140>(v, i);  // row_mirror
+  float bv = lane_value(v, 0);
+  int bi = __builtin_amdgcn_readlane(i, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16) {
+    const float ov = lane_value(v, r);
+    const int oi = __builtin_amdgcn_readlane(i, r);
+    if (ov > bv || (ov == bv && oi < bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  v = bv;
+  i = bi;
+}
+
 // Top-k of one token whose logits a wave holds (lane l: experts l + 64 q,
 // q < V; entries of experts >= E are ignored): k rounds of a wave-wide
-// arg-max over (logit, lower id) by shuffles, so the selection and its
-// order are those of the narrow kernel; then lanes 0..k-1 write the
+// arg-max over (logit, lower id), so the selection and its order are those
+// of the narrow kernel; then lanes 0..k-1 write the
 // selected ids, largest first, and the gates renormalised over them (the
 // full softmax's denominator cancels).
 template <int V>
@@ -203,15 +243,7 @@ __device__ __forceinline__ void wave_topk(const float (&v)[V], int E, int k, int
         bi = e;
       }
     }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, 64);
-      const int oi = __shfl_xor(bi, o, 64);
-      if (ov > bv || (ov == bv && oi < bi)) {
-        bv = ov;
-        bi = oi;
-      }
-    }
+    wave_argmax(bv, bi);
     if ((bi & 63) == lane) taken |= 1u << (bi >> 6);
 #pragma unroll
     for (int jj = 0; jj < 16; ++jj)
@@ -354,20 +386,26 @@ __global__ __launch_bounds__(256) void router_bwd_dx_kernel(
     const int i = lane < k ? idx[t * k + lane] : -1;
     const bool in = i >= 0 && i < E;
     const float g = in ? gates[t * k + lane] : 0.f, d = in ? dgates[t * k + lane] : 0.f;
-    float c = g * d;  // sum over the k <= 16 slots held by lanes 0..15
+    // sum over the k <= 16 slots held by lanes 0..15, read into scalar
+    // registers (v_readlane) and added as a pairwise tree
+    float gd[16];
 #pragma unroll
-    for (int o = 1; o < 16; o <<= 1) c += __shfl_xor(c, o, 64);
-    c = __shfl(c, 0, 64);
+    for (int j = 0; j < 16; ++j) gd[j] = lane_value(g * d, j);
+#pragma unroll
+    for (int w = 1; w < 16; w <<= 1)
+#pragma unroll
+      for (int j = 0; j < 16; j += 2 * w) gd[j] += gd[j + w];
+    const float c = gd[0];
     const float dz = g * (d - c);
     const int id = in ? i : -1;
-    // broadcast the k slots while every lane is active (the row loops below
+    // the k slots, broadcast while every lane is active (the row loops below
     // leave lanes idle when h or EP is short)
     float dzs[16];
     int ids[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      dzs[j] = __shfl(dz, j, 64);
-      ids[j] = j < k ? __shfl(id, j, 64) : -1;
+      dzs[j] = lane_value(dz, j);
+      ids[j] = j < k ? __builtin_amdgcn_readlane(id, j) : -1;
     }
     for (int c0 = lane * V; with_dx && c0 < h; c0 += 64 * V * NV) {
       float acc[NV][V];

@@ -82,3 +82,26 @@ def test_fwd_noalloc_refuses_chunks_beyond_the_scratch(mf):
     mf.memfine_moe_fwd_noalloc(s, C, X, idx, g, W1, W2, Y)
     t.cuda.synchronize()
     assert bool((Y.float() == 0).all())
+
+
+def test_fwd_noalloc_expert_order(mf):
+    """Expert-ordered chunks (launch option chunk_order): the layer's routing
+    tables and the chunk's buffers both come from the static scratch; the
+    same output, bit for bit, as the allocating forward in that order, and
+    nothing allocated."""
+    t = torch()
+    stream = t.cuda.Stream()
+    w = mw.scaled(mw.WORKLOADS[2], T=3000, h=512, F=384)
+    case = mw.make_case(w, 73, with_dy=False)
+    dev = device_case(w, case)
+    try:
+        mf.memfine_set_launch_options(chunk_order=mf.CHUNK_EXPERTS)
+        for C in (2, 5):
+            assert mf.memfine_workspace_bytes(shape_of(w), C, mf.PASS_FWD) <= mf.NOALLOC_SCRATCH_BYTES
+            log(f"no-alloc forward, expert order, C={C}")
+            Y_ref, Y = _fwd_both(mf, w, dev, C, stream)
+            assert np.array_equal(Y, Y_ref)
+            ref = om.moe_fwd(case["X"], case["idx"], case["gates"], case["W1"], case["W2"], C)
+            assert relerr(Y, ref) <= TOL["bf16"]
+    finally:
+        mf.memfine_set_launch_options()
