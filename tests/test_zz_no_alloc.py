@@ -5,6 +5,8 @@ a row, the second with a smaller input, both also within the bf16 tolerance
 of the oracle; nothing is allocated (the torch allocator, the library's pool
 and its per-stream workspace stay as they were); a call whose largest chunk
 needs more than the static scratch is refused before anything runs."""
+import gc
+
 import numpy as np
 import pytest
 
@@ -32,6 +34,10 @@ def _fwd_both(mf, w, dev, C, stream):
     mf.memfine_moe_fwd(s, C, dev["X"], dev["idx"], dev["gates"], dev["W1"], dev["W2"], Y_ref)
     t.cuda.synchronize()
     Y = nan_like((w.T, w.h), t.bfloat16)
+    # tensors of earlier tests that only the cycle collector frees (a caught
+    # exception's traceback holds their frames) go now, not inside the window
+    gc.collect()
+    t.cuda.synchronize()
     torch_before = t.cuda.memory_allocated()
     pool_before = mf.memfine_pool_high_water()
     with t.cuda.stream(stream):
