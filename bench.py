@@ -33,6 +33,7 @@ Prints ONE JSON line (rank 0, N = 1 GPU):
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -396,6 +397,7 @@ def main():
             tps = w.T * n_t / (time.perf_counter() - a)
             alloc = mf.TorchAllocator()
             torch.cuda.synchronize()
+            gc.collect()
             torch.cuda.reset_peak_memory_stats()
             base = torch.cuda.memory_allocated()
             step(Cs, allocator=alloc)
@@ -555,6 +557,7 @@ def sweep_budgets(mf, torch, cfg):
         rc, C, info = mf.memfine_plan(shape, counts, b, bins=w.bins)
         alloc = mf.TorchAllocator()
         torch.cuda.synchronize()
+        gc.collect()
         torch.cuda.reset_peak_memory_stats()
         base = torch.cuda.memory_allocated()
         mf.memfine_moe_fwd(shape, C, dev["X"], idx, gates, dev["W1"], dev["W2"], Y, allocator=alloc)

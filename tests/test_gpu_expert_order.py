@@ -10,6 +10,8 @@ layer's slots grouped by expert, so Y and dX are sums over chunks.
 * the working memory the layer holds at once equals its declared workspace.
 Every output starts as NaN, so an element no chunk writes fails the check.
 """
+import gc
+
 import numpy as np
 import pytest
 
@@ -159,6 +161,7 @@ def test_expert_order_allocator_peak(mf, experts_order):
         alloc = mf.TorchAllocator()
         t.cuda.synchronize()
         t.cuda.empty_cache()
+        gc.collect()                 # no frees of earlier garbage inside the window
         t.cuda.reset_peak_memory_stats()
         base = t.cuda.memory_allocated()
         log(f"expert order allocator peak C={C}")

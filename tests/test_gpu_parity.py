@@ -11,6 +11,8 @@ oracle on the same seeded inputs.
   sampled tokens and sampled weight-gradient columns the oracle computes one
   by one.
 """
+import gc
+
 import numpy as np
 import pytest
 
@@ -415,6 +417,7 @@ def test_allocator_hook_peak_and_oom(mf):
         alloc = mf.TorchAllocator()
         t.cuda.synchronize()
         t.cuda.empty_cache()
+        gc.collect()                 # no frees of earlier garbage inside the window
         t.cuda.reset_peak_memory_stats()
         base = t.cuda.memory_allocated()
         log(f"allocator peak C={C}")
