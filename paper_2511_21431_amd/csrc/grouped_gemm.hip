@@ -60,10 +60,10 @@ constexpr uint32_t kOOB = 0x80000000u;    // byte offset past every buffer's ran
 #endif
 constexpr bool kSchedHints = MEMFINE_SCHED_HINTS;
 // Wave priority while a tile's MFMAs issue (s_setprio), for the
-// register-staged copy loops: there each wave also issues the next K tile's
+// register-staged copy loop: there each wave also issues the next K tile's
 // loads and LDS writes, and the SIMD's arbiter then favours the wave that
-// feeds the matrix core (dgrads 3-6 % faster; the direct-copy loops measured
-// 1-2 % slower with it, so they keep the default priority).
+// feeds the matrix core (3-6 % faster; the direct-copy loops measured 1-2 %
+// slower with it, so they keep the default priority).
 #ifndef MEMFINE_MMA_PRIO
 #define MEMFINE_MMA_PRIO 2
 #endif
@@ -1717,11 +1717,10 @@ __attribute__((amdgpu_waves_per_eu(C::kMinWaves, C::kMinWaves))) void grouped_ge
 // Launches of direct-copy tiles of equal cost run persistent: one workgroup
 // per CU walks ids blockIdx.x, + cus, ..., with the next tile's first copies
 // in flight during the epilogue (after it, where the epilogue loads).  The
-// others run
-// one tile per workgroup: register-staged copies leave no registers to carry
-// a next tile, and weight-gradient tiles (K = the expert's rows) differ in
-// cost, which the hardware's dynamic dispatch balances better than a fixed
-// stride (measured 3-8 % faster).
+// others run one tile per workgroup: register-staged copies (a launch
+// option) leave no registers to carry a next tile, and weight-gradient tiles
+// (K = the expert's rows) differ in cost, which the hardware's dynamic
+// dispatch balances better than a fixed stride (measured 3-8 % faster).
 template <class C, class P>
 constexpr bool kPersistent = C::DIRECT && C::S == 2 && P::kEqualTiles;
 // Weight gradients (direct copies, tile cost = the expert's rows) run
@@ -1973,7 +1972,6 @@ inline double rounds(int tiles, int per_cu) {
 using Big8 = Cfg<256, 256, 2, 4, 2>;        // 8 waves of 128 x 64
 using Big8R = Cfg<256, 256, 2, 4, 2, 128, 0>;  // Big8 with register-staged copies
 using Quarter8 = Cfg<128, 128, 4, 2, 2>;        // quarter tiles of Big8 (8 waves of 32 x 64)
-using Quarter8R = Cfg<128, 128, 4, 2, 2, 128, 0>;
 
 template <typename T, class C> using FC1Fwd = ProbFC1<T, C, false>;
 template <typename T, class C> using FC1Bwd = ProbFC1<T, C, true>;
@@ -2000,27 +1998,14 @@ hipError_t launch_split_cfg(const GemmArgs& g, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Operand copy path per problem: the dgrads (an activation-row operand and a
-// K-strided weight operand) measured 8-16 % faster with register-staged
-// copies; the forward GEMMs and the weight gradients are faster with direct
-// copies into LDS.
-template <template <typename, class> class PT> struct StagedCopies {
-  static constexpr bool value = false;
-};
-template <> struct StagedCopies<ProbFC2Dgrad> {
-  static constexpr bool value = true;
-};
-template <> struct StagedCopies<ProbFC1Dgrad> {
-  static constexpr bool value = true;
-};
-template <> struct StagedCopies<ProbRouterDx> {
-  static constexpr bool value = true;
-};
-
 // Pick the tile shape.  The 256 x 256 tile on 8 waves (one workgroup per CU,
 // two waves per SIMD, 128 x 64 per wave) measured fastest on every workload
 // shape here, from 8k to 65k slots and C = 1..4; the 128 x 128 tile (two
 // workgroups per CU) only serves grids too small to give most CUs a tile.
+// Every problem takes direct copies into LDS: the dgrads (an activation-row
+// operand and a K-strided weight operand) and the router's dX measured 2-8 %
+// faster with them than with register-staged copies, which remain a launch
+// option (MEMFINE_TILE_256_REG).
 template <template <typename, class> class PT>
 hipError_t launch_auto(const GemmArgs& g_in, hipStream_t s) {
   GemmArgs g = g_in;
@@ -2033,12 +2018,8 @@ hipError_t launch_auto(const GemmArgs& g_in, hipStream_t s) {
     default: break;
   }
   if (PT<float, Big8>::grid(g) >= 128) {
-    if (g.split_tail) {
-      if constexpr (StagedCopies<PT>::value) return launch_split_cfg<PT, Big8R, Quarter8R>(g, s);
-      else return launch_split_cfg<PT, Big8, Quarter8>(g, s);
-    }
-    if constexpr (StagedCopies<PT>::value) return launch_cfg<PT, Big8R>(g, s);
-    else return launch_cfg<PT, Big8>(g, s);
+    if (g.split_tail) return launch_split_cfg<PT, Big8, Quarter8>(g, s);
+    return launch_cfg<PT, Big8>(g, s);
   }
   return launch_cfg<PT, Small>(g, s);
 }
