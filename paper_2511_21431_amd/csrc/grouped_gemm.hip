@@ -784,7 +784,7 @@ __device__ __forceinline__ void store_rows(const Accum<C>& acc, T* out, int ld, 
 template <typename T, class C, bool kBwd> struct ProbFC1 {
   typedef ProbFC1 ProbSelf;
   static constexpr bool kEqualTiles = true;  // every tile reduces over the same K
-  static constexpr int kRaster = 4;  // preferred tile order (XCD blocks, row-major)
+  static constexpr int kRaster = 2;  // preferred tile order (XCD blocks of 8 x 4 tiles)
   static constexpr bool kEpilogueLoads = kBwd;  // the epilogue reads global memory
   static constexpr int kHalf = C::WTN / 2;
   // the recomputation's epilogue can stage its stores through LDS (bf16, 32
@@ -969,7 +969,7 @@ template <typename T, class C, bool kBwd> struct ProbFC1 {
 template <typename T, class C> struct ProbFC2 {
   typedef ProbFC2 ProbSelf;
   static constexpr bool kEqualTiles = true;  // every tile reduces over the same K
-  static constexpr int kRaster = 4;  // preferred tile order (XCD blocks, row-major)
+  static constexpr int kRaster = 2;  // preferred tile order (XCD blocks of 8 x 4 tiles)
   static constexpr bool kEpilogueLoads = false;  // the epilogue reads global memory
   typedef KcOp<T, C::BM, C::NW, C::KB, C::DA> OA;
   typedef KcOp<T, C::BN, C::NW, C::KB, C::DB> OB;
@@ -1034,7 +1034,7 @@ template <typename T, class C> struct ProbLogits : ProbFC2<T, C> {
 template <typename T, class C> struct ProbFC2Dgrad {
   typedef ProbFC2Dgrad ProbSelf;
   static constexpr bool kEqualTiles = true;  // every tile reduces over the same K
-  static constexpr int kRaster = 4;  // preferred tile order (XCD blocks, row-major)
+  static constexpr int kRaster = 2;  // preferred tile order (XCD blocks of 8 x 4 tiles)
   static constexpr bool kEpilogueLoads = false;  // the epilogue reads global memory
   typedef KcOp<T, C::BM, C::NW, C::KB, C::DA> OA;
   typedef KsOp<T, C::BN, C::NW, C::KB, C::DB> OB;
@@ -1184,7 +1184,7 @@ template <typename T, class C> struct ProbRouterDx : ProbFC2Dgrad<T, C> {
 template <typename T, class C> struct ProbFC1Dgrad {
   typedef ProbFC1Dgrad ProbSelf;
   static constexpr bool kEqualTiles = true;  // every tile reduces over the same K
-  static constexpr int kRaster = 4;  // preferred tile order (XCD blocks, row-major)
+  static constexpr int kRaster = 2;  // preferred tile order (XCD blocks of 8 x 4 tiles)
   static constexpr bool kEpilogueLoads = false;  // the epilogue reads global memory
   typedef KcOp<T, C::BM, C::NW, C::KB, C::DA> OA;
   typedef KsOp<T, C::BN, C::NW, C::KB, C::DB> OB;
