@@ -438,10 +438,12 @@ __device__ __forceinline__ void mma_tile(const char* As, const char* Bs, Accum<C
   for (int kk = 0; kk < KS; ++kk) {
     const int cu = kk & 1, nx = cu ^ 1;
     if (kk + 1 < KS) {
-#pragma clang loop unroll(full)
-      for (int i = 0; i < C::MB; ++i) a[nx][i] = OA::read(As, wm * C::WTM + i * 32, kk + 1, lane);
+      // B's fragments first: every MFMA of a row i uses all of them, A's
+      // fragment i only its own row
 #pragma clang loop unroll(full)
       for (int j = 0; j < C::NB; ++j) b[nx][j] = OB::read(Bs, wn * C::WTN + j * 32, kk + 1, lane);
+#pragma clang loop unroll(full)
+      for (int i = 0; i < C::MB; ++i) a[nx][i] = OA::read(As, wm * C::WTM + i * 32, kk + 1, lane);
     }
 #pragma clang loop unroll(full)
     for (int i = 0; i < C::MB; ++i)
@@ -457,9 +459,16 @@ __device__ __forceinline__ void mma_tile(const char* As, const char* Bs, Accum<C
 #pragma clang loop unroll(full)
       for (int x = 0; x < kMfma; ++x) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if (x < kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if (kReads <= kMfma) {
+          if (x < kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        } else {
+          // more reads than MFMAs (the weight gradients' two transposed
+          // operands): all of them go out during this step's MFMAs, the
+          // surplus with the first ones, so that none waits at the step's end
+          __builtin_amdgcn_sched_group_barrier(0x100, kReads / kMfma, 0);
+          if (x < kReads % kMfma) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
       }
-      if (kReads > kMfma) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kMfma, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
   }
@@ -495,10 +504,11 @@ __device__ __forceinline__ void mma_tile_carry(const char* As, const char* Bs, A
 #pragma clang loop unroll(full)
   for (int kk = 0; kk + 1 < KS; ++kk) {
     const int cu = kk & 1, nx = cu ^ 1;
-#pragma clang loop unroll(full)
-    for (int i = 0; i < C::MB; ++i) f.a[nx][i] = OA::read(As, wm * C::WTM + i * 32, kk + 1, lane);
+    // B's fragments first, as in mma_tile
 #pragma clang loop unroll(full)
     for (int j = 0; j < C::NB; ++j) f.b[nx][j] = OB::read(Bs, wn * C::WTN + j * 32, kk + 1, lane);
+#pragma clang loop unroll(full)
+    for (int i = 0; i < C::MB; ++i) f.a[nx][i] = OA::read(As, wm * C::WTM + i * 32, kk + 1, lane);
 #pragma clang loop unroll(full)
     for (int i = 0; i < C::MB; ++i)
 #pragma clang loop unroll(full)
@@ -516,9 +526,16 @@ __device__ __forceinline__ void mma_tile_carry(const char* As, const char* Bs, A
 #pragma clang loop unroll(full)
       for (int x = 0; x < kMfma; ++x) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if (x < kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if (kReads <= kMfma) {
+          if (x < kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        } else {
+          // more reads than MFMAs (the weight gradients' two transposed
+          // operands): all of them go out during this step's MFMAs, the
+          // surplus with the first ones, so that none waits at the step's end
+          __builtin_amdgcn_sched_group_barrier(0x100, kReads / kMfma, 0);
+          if (x < kReads % kMfma) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
       }
-      if (kReads > kMfma) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kMfma, 0);
     }
   }
   if constexpr (kPrio > 0) __builtin_amdgcn_s_setprio(0);
