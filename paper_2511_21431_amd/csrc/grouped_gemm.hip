@@ -7,11 +7,11 @@
 // over one expert at a time and multiplied by 32x32 MFMA instructions
 // (v_mfma_f32_32x32x16_bf16, or v_mfma_f32_32x32x2f32 on the fp32 path).
 //
-// Operand movement.  Operand tiles go from HBM into LDS either directly with
-// buffer_load ... lds (16 bytes per lane, no staging registers: forward GEMMs
-// and weight gradients) or through registers (buffer_load into VGPRs during
-// the previous K tile's multiply, then ds_write_b128: the two dgrads, where
-// that measured faster).  Buffer resources bound each tensor, so rows past
+// Operand movement.  Operand tiles go from HBM into LDS directly with
+// buffer_load ... lds (16 bytes per lane, no staging registers), or, as a
+// launch option, through registers (buffer_load into VGPRs during the
+// previous K tile's multiply, then ds_write_b128).  Buffer resources bound
+// each tensor, so rows past
 // the end of a tensor, ragged tails and the K tail of a weight-gradient tile
 // read as zero in hardware.
 // Two LDS layouts serve the two ways an operand can sit in HBM:
@@ -37,8 +37,9 @@
 // runs while the waves multiply tile k, with one barrier per K step.
 //
 // Tile order.  Workgroups are dealt round-robin to the 8 XCDs; the
-// row-grouped GEMMs map ids to tiles in blocks of 32 per XCD so that the
-// tiles one XCD holds at once share operand K-slices in its L2, and launches
+// row-grouped GEMMs map ids to tiles in blocks of 32 per XCD (8 m-tiles x 4
+// n-tiles) so that the tiles one XCD holds at once share operand K-slices in
+// its L2, and launches
 // of equal-cost direct-copy tiles run persistent (one workgroup per CU, the
 // next tile's first copies in flight during the epilogue).
 //
