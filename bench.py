@@ -20,6 +20,9 @@ Prints ONE JSON line (rank 0, N = 1 GPU):
                the launch stream inside the timed region)
   gemm         every grouped GEMM's algorithmic TFLOP/s and share of the
                bf16 peak, beside the 60 % target
+  hbm_kernels  the memory-bound steps' algorithmic GB/s against 8 TB/s and
+               against a plain streaming copy measured in the same run
+               (hbm_copy_reference)
   cpu_baseline the fp64 oracle on the host cores, on a bounded token sample
   chunks_sweep tokens/s and measured peak activation bytes for every chunk
                count of the workload, beside the memory-model predictions
@@ -60,6 +63,7 @@ BUDGET_SWEEP = {5: [4 * 10**9, 8 * 10**9, 16 * 10**9, 32 * 10**9, 64 * 10**9],
 ROUTER_WIDTH = {4: 256, 5: 256}
 GEMMS = ("fc1", "fc2", "fc1_recompute", "fc2_dgrad", "fc2_wgrad", "fc1_wgrad", "fc1_dgrad")
 GEMM_TARGET = 0.60   # share of the bf16 MFMA peak the grouped GEMMs aim for
+HBM_KERNELS = ("combine", "unpermute")  # the memory-bound steps
 
 
 def log(msg):
@@ -382,6 +386,21 @@ def main():
     log(f"[bench] {ms_per_step:.3f} ms/step, {tokens_per_s:.0f} tokens/s, dominant {dominant} "
         f"avg {avg_ms:.3f} ms {achieved_tflops:.1f} TFLOP/s {achieved_gbs:.1f} GB/s ({bound}-bound)")
 
+    # ---- what a plain streaming copy reaches on this part: the reference for
+    # the memory-bound kernels besides the 8 TB/s nameplate
+    copy_ref = hbm_copy_reference(torch)
+    hbm_kernels = {}
+    for k in HBM_KERNELS:
+        v = prof_all.get(k)
+        if v and v["total_ms"] > 0:
+            gbs = v["bytes"] / (v["total_ms"] * 1e-3) / 1e9
+            hbm_kernels[k] = {"ms": round(v["total_ms"], 4), "gbs": round(gbs, 1),
+                              "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4),
+                              "frac_of_copy": round(gbs / copy_ref["gbs"], 4)}
+    log(f"[bench] streaming copy: {copy_ref['gbs']:.0f} GB/s; " +
+        ", ".join(f"{k} {v['gbs']:.0f} GB/s ({v['frac_of_copy']:.2f} of it)"
+                  for k, v in hbm_kernels.items()))
+
     # ---- chunk-count sweep: throughput and measured peak activation memory
     sweep = []
     if not args.no_sweep:
@@ -506,6 +525,8 @@ def main():
                                  "gbs": round(v["bytes"] / max(v["total_ms"], 1e-9) / 1e6, 1)}
                              for k, v in prof_all.items()},
         "layer_roofline_frac": round(layer_bound_ms(prof_all, peak) / ms_per_step, 4),
+        "hbm_copy_reference": copy_ref,
+        "hbm_kernels": hbm_kernels,
         "chunks_sweep": sweep,
         "budget_sweep": budget_sweep,
         "budget_sweep_workload3": budget_sweep3,
@@ -515,6 +536,30 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def hbm_copy_reference(torch, nbytes=1 << 30, reps=5):
+    """Best of `reps` device-to-device copies of `nbytes` (read + write, both
+    far beyond the last-level cache), timed with events: the bandwidth a plain
+    streaming kernel reaches on this part."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    del src, dst
+    ms = min(times)
+    return {"gbs": round(2.0 * nbytes / (ms * 1e-3) / 1e9, 1), "bytes_moved": 2 * nbytes,
+            "ms": round(ms, 4), "kernel": "torch copy_ of a 1 GiB fp32 tensor (best of 5)",
+            "frac_of_peak": round(2.0 * nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
 
 
 def gemm_table(prof, peak_tflops):
