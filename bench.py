@@ -835,12 +835,31 @@ def cpu_baseline(w, idx_np, gates_np, dev, C, target_s):
         if elapsed >= target_s / 3 or Ts >= w.T:
             break
         Ts = min(w.T, int(Ts * max(2.0, target_s / max(elapsed, 1e-3))))
+    out = {"value": round(Ts / elapsed, 2), "unit": "tokens/s", "cores": threads,
+           "kind": "oracle", "cpu": host_cpu(),
+           "sample": f"first {Ts} of {w.T} tokens, fp64 NumPy oracle fwd + chunked-recompute "
+                     f"bwd at C={C}, {elapsed:.1f} s"}
+    if w.h * w.F <= 2048 * 1408:
+        # the small workloads also on one host thread, on a sample sized for
+        # about a third of the time budget at the measured many-thread rate
+        try:
+            from threadpoolctl import threadpool_limits
+            T1 = max(16, min(Ts, int(Ts / elapsed * target_s / 3 / max(threads, 1))))
+            with threadpool_limits(limits=1):
+                X = dev["X"][:T1].double().cpu().numpy()
+                dY = dev["dY"][:T1].double().cpu().numpy()
+                a = time.perf_counter()
+                om.moe_fwd(X, idx_np[:T1], gates_np[:T1], W1, W2, C)
+                om.moe_bwd(X, idx_np[:T1], gates_np[:T1], W1, W2, dY, C)
+                e1 = time.perf_counter() - a
+            out["one_thread"] = {"value": round(T1 / e1, 2), "unit": "tokens/s", "cores": 1,
+                                 "sample": f"first {T1} of {w.T} tokens, {e1:.1f} s"}
+            log(f"[bench] cpu baseline, one thread: {T1} tokens in {e1:.2f} s")
+        except ImportError:
+            pass
     del W1, W2
     torch.cuda.synchronize()
-    return {"value": round(Ts / elapsed, 2), "unit": "tokens/s", "cores": threads,
-            "kind": "oracle", "cpu": host_cpu(),
-            "sample": f"first {Ts} of {w.T} tokens, fp64 NumPy oracle fwd + chunked-recompute "
-                      f"bwd at C={C}, {elapsed:.1f} s"}
+    return out
 
 
 if __name__ == "__main__":
