@@ -20,6 +20,8 @@ Prints ONE JSON line (rank 0, N = 1 GPU):
                the launch stream inside the timed region)
   gemm         every grouped GEMM's algorithmic TFLOP/s and share of the
                bf16 peak, beside the 60 % target
+  clock        the graphics clock through the timed steps (amdsmi), and the
+               layer's executed flops against the peak scaled to it
   hbm_kernels  the memory-bound steps' algorithmic GB/s against 8 TB/s and
                against a plain streaming copy measured in the same run
                (hbm_copy_reference)
@@ -357,13 +359,15 @@ def main():
     mf.memfine_profile_begin([dominant])
     torch.cuda.synchronize()
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    t0 = time.perf_counter()
-    ends[0].record()
-    for i in range(args.steps):
-        step()
-        ends[i + 1].record()   # per-step GPU time between consecutive step ends
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
+    with ClockSampler() as clock:
+        t0 = time.perf_counter()
+        ends[0].record()
+        for i in range(args.steps):
+            step()
+            ends[i + 1].record()   # per-step GPU time between consecutive step ends
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+    clock = clock.summary()
     prof = mf.memfine_profile_end()
     step_ms = sorted(a.elapsed_time(b) for a, b in zip(ends, ends[1:]))
     ms_per_step = (t1 - t0) * 1e3 / args.steps
@@ -383,6 +387,9 @@ def main():
     achieved = achieved_gbs if bound == "hbm" else achieved_tflops
     traffic = read_traffic(dominant, f"cfg{cfg}")
     executed_flops = 22.0 * w.N * w.h * w.F
+    if clock:
+        log(f"[bench] clock during the timed steps: mean {clock['mean_ghz']:.2f} GHz "
+            f"(min {clock['min_ghz']:.2f}, max {clock['max_ghz']:.2f}, {clock['samples']} samples)")
     log(f"[bench] {ms_per_step:.3f} ms/step, {tokens_per_s:.0f} tokens/s, dominant {dominant} "
         f"avg {avg_ms:.3f} ms {achieved_tflops:.1f} TFLOP/s {achieved_gbs:.1f} GB/s ({bound}-bound)")
 
@@ -509,6 +516,13 @@ def main():
         # time, as a share of the bf16 peak: not a hardware MFMA counter
         "layer_flops_frac_of_peak": round(executed_flops / (ms_per_step * 1e-3) / 1e12 / peak, 4),
         "layer_tflops": round(executed_flops / (ms_per_step * 1e-3) / 1e12, 1),
+        # the clock the chip held during the timed steps, and the layer's
+        # executed flops against the bf16 peak scaled to that clock (the
+        # 2.5 PFLOP/s figure assumes 2.4 GHz)
+        "clock": clock,
+        "layer_flops_frac_of_peak_at_clock": (
+            round(executed_flops / (ms_per_step * 1e-3) / 1e12 / (peak * clock["mean_ghz"] / 2.4), 4)
+            if clock else None),
         "gemm": gemm_table(prof_all, peak),
         "gemm_target_frac_of_peak": GEMM_TARGET,
         "roofline": {"kernel": dominant, "bound": bound, "achieved": round(achieved, 1),
@@ -536,6 +550,56 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+class ClockSampler:
+    """The GPU's current graphics clock (amdsmi), sampled every `period`
+    seconds by a daemon thread while the timed steps run.  Everything amdsmi
+    does happens on that thread, so a failing or slow query never holds up
+    the measurement; without amdsmi the summary is None."""
+
+    def __init__(self, period=0.01):
+        import threading
+        self.period, self.samples = period, []
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+
+    def _run(self):
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+        except Exception:
+            return
+        try:
+            h = amdsmi.amdsmi_get_processor_handles()[0]
+            while not self._stop.is_set():
+                mhz = amdsmi.amdsmi_get_clock_info(h, amdsmi.AmdSmiClkType.GFX)["clk"]
+                if isinstance(mhz, (int, float)):
+                    self.samples.append(float(mhz))
+                self._stop.wait(self.period)
+        except Exception:
+            pass
+        finally:
+            try:
+                amdsmi.amdsmi_shut_down()
+            except Exception:
+                pass
+
+    def __enter__(self):
+        self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._thread.join(timeout=1.0)
+
+    def summary(self):
+        v = list(self.samples)
+        if not v:
+            return None
+        return {"mean_ghz": round(sum(v) / len(v) / 1e3, 3), "min_ghz": round(min(v) / 1e3, 3),
+                "max_ghz": round(max(v) / 1e3, 3), "samples": len(v),
+                "source": "amdsmi current GFX clock every 10 ms during the timed steps"}
 
 
 def hbm_copy_reference(torch, nbytes=1 << 30, reps=5):
