@@ -1,7 +1,7 @@
-"""The benchmark's host-side counter summaries (no GPU): HBM traffic per FC1
+"""The benchmark's host-side summaries (no GPU): HBM traffic per FC1
 weight-gradient launch from FETCH_SIZE / WRITE_SIZE runs scaled by the 1 GiB
 calibration pass, and the per-GEMM MFMA table, on small hand-made counter
-files in rocprofv3's CSV layout."""
+files in rocprofv3's CSV layout; the clock sampler's summary."""
 import csv
 import json
 
@@ -83,3 +83,23 @@ def test_mfma_summary(tmp_path):
     a = agg["fc1"]
     assert a["util"] == pytest.approx(512000.0 / (1000.0 * 1024.0))
     assert a["tflops"] == pytest.approx(1e9 * 512 / 100e-6 / 1e12)
+
+
+def test_clock_sampler_summary():
+    """The clock summary: None without samples (no amdsmi, no GPU), else the
+    mean, range and count of the sampled MHz values in GHz."""
+    c = bench.ClockSampler()
+    assert c.summary() is None
+    c.samples = [1800.0, 1700.0, 1600.0]
+    s = c.summary()
+    assert s["mean_ghz"] == pytest.approx(1.7) and s["min_ghz"] == pytest.approx(1.6)
+    assert s["max_ghz"] == pytest.approx(1.8) and s["samples"] == 3
+
+
+def test_clock_sampler_without_gpu_ends():
+    """On a host without a GPU the sampler thread ends at once and the timed
+    block runs as usual."""
+    import time
+    with bench.ClockSampler() as c:
+        time.sleep(0.05)
+    assert not c._thread.is_alive() or c.summary() is None
