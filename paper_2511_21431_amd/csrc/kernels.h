@@ -7,12 +7,15 @@
 namespace memfine {
 
 // Slots handled by one workgroup of the dispatch histogram / scatter kernels:
-// 256 (one round of the scatter) while that needs at most 4096 workgroups,
+// 256 (one round of the scatter) while that needs at most 128 workgroups,
 // else the smallest power-of-two multiple that does, which bounds the
-// per-workgroup count tables at E * 4096 entries.
+// per-workgroup count tables at E * 128 entries.  Every scatter workgroup
+// reads all E x nb block counts for its prefix: at 131072 slots, 512
+// workgroups of 256 slots spent most of the dispatch's 57 us on that read;
+// 128 of 1024 take 25 us.
 inline int dispatch_slots_per_block(int64_t n) {
   int64_t spb = 256;
-  while ((n + spb - 1) / spb > 4096) spb *= 2;
+  while ((n + spb - 1) / spb > 128) spb *= 2;
   return (int)spb;
 }
 inline int dispatch_blocks(int64_t n) {
