@@ -20,6 +20,8 @@ Prints ONE JSON line (rank 0, N = 1 GPU):
                the launch stream inside the timed region)
   gemm         every grouped GEMM's algorithmic TFLOP/s and share of the
                bf16 peak, beside the 60 % target
+  gemm_reference  the vendor library's batched bf16 GEMM at FC1's shape
+               (uniform rows per expert, no gather) beside FC1's own rate
   clock        the graphics clock through the timed steps (amdsmi), and the
                layer's executed flops against the peak scaled to it
   hbm_kernels  the memory-bound steps' algorithmic GB/s against 8 TB/s and
@@ -404,6 +406,16 @@ def main():
             hbm_kernels[k] = {"ms": round(v["total_ms"], 4), "gbs": round(gbs, 1),
                               "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4),
                               "frac_of_copy": round(gbs / copy_ref["gbs"], 4)}
+    gemm_ref = None
+    if w.dtype == "bf16":
+        rows_ref = max(256, -(-w.T // C) * w.k // w.E)
+        gemm_ref = gemm_reference(torch, w.E, rows_ref, 2 * w.F, w.h)
+        fc1 = prof_all.get("fc1")
+        if fc1 and fc1["total_ms"] > 0:
+            gemm_ref["fc1_tflops"] = round(fc1["flops"] / (fc1["total_ms"] * 1e-3) / 1e12, 1)
+            gemm_ref["fc1_frac_of_reference"] = round(gemm_ref["fc1_tflops"] / gemm_ref["tflops"], 4)
+        log(f"[bench] vendor batched GEMM at FC1's shape ({w.E} x {rows_ref} rows): "
+            f"{gemm_ref['tflops']:.0f} TFLOP/s; FC1 {gemm_ref.get('fc1_tflops')} TFLOP/s")
     log(f"[bench] streaming copy: {copy_ref['gbs']:.0f} GB/s; " +
         ", ".join(f"{k} {v['gbs']:.0f} GB/s ({v['frac_of_copy']:.2f} of it)"
                   for k, v in hbm_kernels.items()))
@@ -540,6 +552,7 @@ def main():
                              for k, v in prof_all.items()},
         "layer_roofline_frac": round(layer_bound_ms(prof_all, peak) / ms_per_step, 4),
         "hbm_copy_reference": copy_ref,
+        "gemm_reference": gemm_ref,
         "hbm_kernels": hbm_kernels,
         "chunks_sweep": sweep,
         "budget_sweep": budget_sweep,
@@ -600,6 +613,31 @@ class ClockSampler:
         return {"mean_ghz": round(sum(v) / len(v) / 1e3, 3), "min_ghz": round(min(v) / 1e3, 3),
                 "max_ghz": round(max(v) / 1e3, 3), "samples": len(v),
                 "source": "amdsmi current GFX clock every 10 ms during the timed steps"}
+
+
+def gemm_reference(torch, E, rows, n, kdim, reps=5):
+    """Best of `reps` vendor batched bf16 GEMMs (torch.bmm, contiguous
+    operands) of E x [rows x kdim] @ [kdim x n]: FC1's shape with every
+    expert given the same row count and no gather, the dense-library
+    reference for the grouped GEMMs under this part's power limit."""
+    a = torch.randn(E, rows, kdim, device="cuda").bfloat16()
+    b = (torch.randn(E, kdim, n, device="cuda") * 0.02).bfloat16().contiguous()
+    c = torch.bmm(a, b)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        c = torch.bmm(a, b)
+        e1.record()
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    del a, b, c
+    ms = min(times)
+    tf = 2.0 * E * rows * n * kdim / (ms * 1e-3) / 1e12
+    return {"tflops": round(tf, 1), "ms": round(ms, 4), "experts": E, "rows_per_expert": rows,
+            "n": n, "k": kdim, "kernel": "torch.bmm bf16 (vendor BLAS), best of 5"}
 
 
 def hbm_copy_reference(torch, nbytes=1 << 30, reps=5):
