@@ -296,3 +296,19 @@ def test_router_limits_and_null_pointers_rejected_on_host():
     assert L.memfine_router_bwd(ctypes.byref(ok), *([fake] * 7), 2, 0, None, None) == -1
     assert L.memfine_router_bwd(ctypes.byref(ok), *([fake] * 7), 0, -1, None, None) == -1
     assert L.memfine_router_fwd(None, fake, fake, fake, fake, None, None) == -1
+
+
+def test_missing_library_fails_loudly():
+    """Without the built library every entry point raises: there is no CPU
+    fallback behind the binding."""
+    import subprocess
+    import sys
+    code = ("import paper_2511_21431_amd._lib as L\n"
+            "L.LIB_PATH = '/nonexistent/libmemfine.so'\n"
+            "try:\n"
+            "    L.memfine_status_str(0)\n"
+            "except ImportError as e:\n"
+            "    print('raised', 'no fallback' in str(e))\n")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                         cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))), timeout=300)
+    assert "raised True" in out.stdout, out.stdout + out.stderr
