@@ -483,9 +483,9 @@ def test_full_size_sampled(mf, cfg, C, order):
         mf.memfine_set_launch_options()
 
 
-def _full_size_sampled(mf, cfg, C):
+def _full_size_sampled(mf, cfg, C, w=None):
     t = torch()
-    w = W[cfg]
+    w = W[cfg] if w is None else w
     log(f"full-size cfg{cfg} C={C}: generating inputs")
     idx, gates = mw.make_routing(w, cfg)
     dev = mw.make_tensors_device(w, cfg, "cuda")
@@ -535,3 +535,21 @@ def _full_size_sampled(mf, cfg, C):
     log(f"  cfg{cfg} C={C}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
     for key, e in errs.items():
         assert e <= tol, (key, e)
+
+
+# The largest token count the ABI takes at h = 7168 in bf16: X and dY are
+# addressed with 31-bit byte offsets, and T h 2 = 2147475456 leaves 8 KB
+# below 2^31, so the last token's row sits at the top of that range.
+T_MAX_H7168 = (2 ** 31 - 1) // (7168 * 2)
+
+
+def test_largest_token_count_sampled(mf):
+    """Sampled parity (the first and the last token among them) at the
+    largest T for h = 7168, k = 1, 8 experts, C = 2; one more token is
+    refused on the host."""
+    w = mw.scaled(W[4], T=T_MAX_H7168, E=8, k=1)
+    _full_size_sampled(mf, 4, 2, w=w)
+    big = mf.make_shape(T_MAX_H7168 + 1, 7168, 2048, 8, 1, mf.BF16)
+    with pytest.raises(mf.MemfineError):
+        mf.memfine_workspace_bytes(big, 2, mf.PASS_FWD)
+
