@@ -29,6 +29,10 @@ CASES = {
     "cfg3-like": (mw.scaled(W[3], T=1024, h=384, F=448), (1, 3, 8)),
     "cfg4-like": (mw.scaled(W[4], T=256, h=448, F=128), (2, 4, 256)),
     "cfg5-like": (mw.scaled(W[5], T=512, h=128, F=192), (1, 8, 16)),
+    # the ABI's largest expert count: one wave per expert can no longer hold
+    # the table, most experts have no row and chunks hold hundreds of them
+    "many-1024": (mw.Workload("many-1024", T=640, h=128, F=192, E=1024, k=3, dtype="bf16",
+                              routing="dirichlet"), (1, 3)),
 }
 
 

@@ -153,10 +153,11 @@ def test_layer_parity(mf, name, C):
         assert e <= tol, (key, e)
 
 
-@pytest.mark.parametrize("E,C", [(80, 1), (80, 3), (200, 2)])
+@pytest.mark.parametrize("E,C", [(80, 1), (80, 3), (200, 2), (1024, 2)])
 def test_layer_parity_many_experts(mf, E, C):
     """More experts than one wave's lanes: the GEMMs locate their row tiles
-    by walking the experts instead of a one-wave table."""
+    by walking the experts instead of a one-wave table (up to the ABI's
+    1024 experts, most of them with no row)."""
     w = mw.Workload(f"many-{E}", T=640, h=128, F=192, E=E, k=3, dtype="bf16", routing="dirichlet")
     case = mw.make_case(w, 17 + E)
     dev = device_case(w, case)
