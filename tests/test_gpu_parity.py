@@ -9,7 +9,7 @@ oracle on the same seeded inputs.
   the whole layer bitwise deterministic run to run;
 * full-size workloads in the launch configuration the benchmark times, on
   sampled tokens and sampled weight-gradient columns the oracle computes one
-  by one.
+  by one, and on 512 tokens plus whole experts' weight gradients.
 """
 import gc
 
@@ -536,6 +536,60 @@ def _full_size_sampled(mf, cfg, C, w=None):
     log(f"  cfg{cfg} C={C}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
     for key, e in errs.items():
         assert e <= tol, (key, e)
+
+
+# 512 seeded tokens (the first and the last among them) and whole weight
+# gradients of the hottest, median and coldest experts, at the planner's chunk
+# counts of workloads 3 (C = 8), 4 (C = 4) and 5 (C = 8).  Each token's Y, dX and
+# dgates depend on that token's row and slots only (Eq. (4)/(5) per token),
+# so the oracle's forward and backward run on the sub-batch of those tokens;
+# an expert's dW sums over all its slots (oracle.moe.moe_dW_expert).  The
+# hot expert of workload 5 (524288 slots, about two minutes of fp64 host
+# work in whole) is checked on sampled columns by test_full_size_sampled.
+@pytest.mark.parametrize("cfg,C", [(3, 8), (4, 4), (5, 8)])
+def test_full_size_512_tokens_whole_dW(mf, cfg, C):
+    t = torch()
+    w = W[cfg]
+    log(f"512-token check cfg{cfg} C={C}: generating inputs")
+    idx, gates = mw.make_routing(w, cfg)
+    dev = mw.make_tensors_device(w, cfg, "cuda")
+    dev["idx"] = t.from_numpy(idx).cuda()
+    dev["gates"] = t.from_numpy(gates).cuda()
+    log(f"512-token check cfg{cfg} C={C}: fwd + bwd")
+    Y = run_fwd(w, dev, C)
+    B = run_bwd(w, dev, C)
+    t.cuda.synchronize()
+    rng = np.random.default_rng(2000 + cfg)
+    toks = np.array(sorted(set(rng.choice(w.T - 2, size=510, replace=False) + 1) |
+                           {0, w.T - 1}), dtype=np.int64)
+    assert len(toks) == 512
+    X = dev["X"].float().cpu().numpy()
+    dY = dev["dY"].float().cpu().numpy()
+    W1 = dev["W1"].float().cpu().numpy()
+    W2 = dev["W2"].float().cpu().numpy()
+    tol = TOL[w.dtype]
+    log(f"512-token check cfg{cfg} C={C}: oracle on the 512-token sub-batch")
+    Y_ref = om.moe_fwd(X[toks], idx[toks], gates[toks], W1, W2, 1)
+    R = om.moe_bwd(X[toks], idx[toks], gates[toks], W1, W2, dY[toks], 1)
+    tk = t.from_numpy(toks).cuda()
+    errs = {"Y": relerr(host(Y[tk]), Y_ref), "dX": relerr(host(B["dX"][tk]), R["dX"]),
+            "dgates": relerr(host(B["dgates"][tk]), R["dgates"])}
+    del R
+    counts = np.bincount(idx.reshape(-1), minlength=w.E)
+    order = np.argsort(-counts, kind="stable")
+    experts = [int(order[w.E // 2]), int(order[-1])]
+    if cfg != 5:
+        experts.insert(0, int(order[0]))
+    for e in experts:
+        log(f"512-token check cfg{cfg} C={C}: whole dW of expert {e} ({int(counts[e])} slots)")
+        d1, d2 = om.moe_dW_expert(X, idx, gates, W1, W2, dY, e)
+        errs[f"dW1[{e}]"] = relerr(host(B["dW1"][e]), d1)
+        errs[f"dW2[{e}]"] = relerr(host(B["dW2"][e]), d2)
+    log(f"  cfg{cfg} C={C}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    for key, e in errs.items():
+        assert e <= tol, (key, e)
+    del X, dY, W1, W2, dev, Y, B
+    gc.collect()
 
 
 # The largest token count the ABI takes at h = 7168 in bf16: X and dY are
