@@ -35,16 +35,22 @@ Readings (the paper is ambiguous here)
   layer with m_g = t = c = b = 1.
 * Table 2 glosses e_n as an FFN size, but it sits in the router-output row;
   it is read as the router's logit width.  It only enters the non-MoE term.
+* Eq. (1)'s four optimizer-state copies of D_opt bytes per weight are read
+  as the fp32 state mixed-precision Adam keeps per bf16 weight: the master
+  weight, its gradient and the two moment estimates (D_para = D_grad = 2,
+  D_opt = 4: 20 bytes per weight).
 
-Pins: Table 2's rows must add up to its printed Total row and to Eq. (2);
+Pins: Eq. (1) equals the bytes a bf16 model trained with Adam holds, counted
+on real tensors after one optimizer step (the reading above); Table 2's
+rows must add up to its printed Total row and to Eq. (2);
 the Table 4 percentages printed in Section 5 (48.03 %, 83.84 %); the 1/C
 scaling of the chunked MoE term against Table 4's three activation figures;
 hand-worked Eq. (8)/(9) tables; the threshold method selects, for every s'',
 the same bin as Eq. (9) followed by the bin choice, and that bin keeps Eq. (3)
 while the next smaller one breaks it.  The absolute 22.9 GB of Table 4 is
 parity unpinned: the received-slot count and the attention shapes of that
-run are not printed.  Eq. (1) is parity unpinned as well: the per-module
-weight sizes behind Table 4's static memory are not printed.
+run are not printed.  So are Table 4's absolute static-memory figures: the
+per-module weight sizes and layer placement behind them are not printed.
 """
 from __future__ import annotations
 
@@ -59,9 +65,8 @@ def _F(x) -> Fraction:
 # --- Eq. (1) ----------------------------------------------------------------
 def static_memory(S_para: Iterable[int], v: int, l: int,
                   D_para: int = 2, D_grad: int = 2, D_opt: int = 4) -> Fraction:
-    """Eq. (1): weights + gradients + four optimizer-state copies.  Parity
-    unpinned: the paper prints no per-module weight sizes S_i to check it
-    against, so only its C counterpart is compared with it."""
+    """Eq. (1): weights + gradients + four optimizer-state copies, over the
+    v l copies of the modules' weights S_i held by one GPU."""
     S = sum(_F(s) for s in S_para)
     return D_para * v * l * S + D_grad * v * l * S + 4 * D_opt * v * l * S
 

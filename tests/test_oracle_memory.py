@@ -132,3 +132,43 @@ def test_m_g():
 @pytest.mark.parametrize("T,C,expect", [(8, 3, 3), (8192, 4, 2048), (5, 8, 1), (10, 4, 3)])
 def test_max_chunk_tokens(T, C, expect):
     assert mm.max_chunk_tokens(T, C) == expect
+
+
+def _adam_state_bytes(sizes, copies):
+    """Bytes a mixed-precision Adam training state holds for `copies` sets of
+    weight tensors of the given element counts, measured on real tensors:
+    bf16 weights with their bf16 gradients from a backward pass, fp32 master
+    weights with fp32 gradients, and torch.optim.Adam's state after one step
+    (its per-weight tensors; the scalar step counters are not per-weight
+    memory)."""
+    import torch
+    torch.manual_seed(0)
+    weights = [torch.randn(n, dtype=torch.bfloat16, requires_grad=True)
+               for _ in range(copies) for n in sizes]
+    sum((w.float() ** 2).sum() for w in weights).backward()
+    master = [w.detach().float().clone().requires_grad_() for w in weights]
+    for m, w in zip(master, weights):
+        m.grad = w.grad.float()
+    opt = torch.optim.Adam(master, lr=1e-3)
+    opt.step()
+    held = [*weights, *(w.grad for w in weights), *master, *(m.grad for m in master)]
+    for m in master:
+        held += [v for v in opt.state[m].values()
+                 if torch.is_tensor(v) and v.shape == m.shape]
+    assert all(t is not None for t in held)
+    return sum(t.numel() * t.element_size() for t in held)
+
+
+@pytest.mark.parametrize("sizes,v,l", [([128, 128, 8], 1, 1), ([96, 40, 7, 1], 2, 3),
+                                       ([1000], 4, 1)])
+def test_static_memory_is_mixed_precision_adam_state(sizes, v, l):
+    """Eq. (1) against the memory that a bf16 model trained with Adam holds,
+    counted on real tensors (torch on the CPU): weights (D_para = 2) and
+    gradients (D_grad = 2) in bf16, and four fp32 copies per weight
+    (D_opt = 4): the master weight, its gradient and Adam's two moment
+    estimates.  v l copies of the modules' weights stand for the v virtual
+    stages of l layers.  A wrong factor or a dropped term of Eq. (1) changes
+    the count."""
+    got = mm.static_memory(sizes, v, l)
+    assert got == _adam_state_bytes(sizes, v * l)
+    assert got == 20 * v * l * sum(sizes)
