@@ -83,6 +83,14 @@ constexpr int kDirectPrio = MEMFINE_DIRECT_PRIO;
 #define MEMFINE_CARRY_STEP 1
 #endif
 constexpr bool kCarryStep = MEMFINE_CARRY_STEP;
+// Weight gradients adding into dW: 1 = the epilogue loads the old values and
+// adds them to the tile's sum; 0 = the accumulators start from them, loaded
+// before the tile's first MFMA (that wait also waits for the previous tile's
+// stores, which the next tile's first K steps otherwise hide).
+#ifndef MEMFINE_DW_ADD_IN_EPILOGUE
+#define MEMFINE_DW_ADD_IN_EPILOGUE 1
+#endif
+constexpr bool kDwAddInEpilogue = MEMFINE_DW_ADD_IN_EPILOGUE;
 // s_waitcnt lgkmcnt(0): this wave's LDS reads have returned
 __device__ __forceinline__ void wait_lgkm0() {
   __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
@@ -1293,7 +1301,7 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
   __device__ __forceinline__ bool acc_of(const Tile& t) const {
     return kAcc < 0 ? t.acc != 0 : kAcc == 1;
   }
-  static constexpr bool kAccLoads = kAcc != 0;
+  static constexpr bool kAccLoads = kAcc != 0 && !kDwAddInEpilogue;
   __host__ __device__ static int tiles_per_expert(const GemmArgs& g) {
     return ((M(g) + C::BM - 1) / C::BM) * ((N(g) + C::BN - 1) / C::BN);
   }
@@ -1425,13 +1433,15 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
 #pragma clang loop unroll(full)
     for (int d = 0; d < D; ++d) load_tokens(d, wave, lane, tok[d]);
   }
-  // Accumulating into dW: the accumulators start from the old dW values,
-  // loaded with the tile's first operand copies (their latency overlaps),
-  // so the epilogue only stores.  Rows past the tile and runs past N load
-  // from clamped in-range addresses; those accumulators are never stored.
+  // Accumulating into dW: by default the accumulators start at zero and the
+  // epilogue adds the old dW values (dW = old + this launch's sum).  Built
+  // with MEMFINE_DW_ADD_IN_EPILOGUE=0 they start from the old values instead,
+  // loaded with the tile's first operand copies.  Rows past the tile and runs
+  // past N load from clamped in-range addresses; those accumulators are
+  // never stored.
   __device__ __forceinline__ void init_acc(const GemmArgs& g, const Tile& t, Accum<C>& acc, int wm,
                                           int wn, int lane) const {
-    if (!acc_of(t)) {
+    if (kDwAddInEpilogue || !acc_of(t)) {
       zero_acc(acc);
       return;
     }
@@ -1488,8 +1498,10 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
       for (int i = 0; i < IG; ++i) tok[d][i] = tok[d + 1][i];
     load_tokens(kt + D, wave, lane, tok[D - 1]);  // D tiles ahead
   }
-  // Vector-memory instructions epilogue() issues: every one, whatever the
-  // tile's extent (elements outside it get an offset past the range).
+  // Vector-memory stores epilogue() issues: every one, whatever the tile's
+  // extent (elements outside it get an offset past the range).  When it adds
+  // into dW it also loads the old values and waits for them, so the loads
+  // are retired, with everything issued before them, when it returns.
   static constexpr int kEpiStores = C::MB * C::NB * 4;
   __device__ __forceinline__ void epilogue(const GemmArgs& g, const Tile& t, const Accum<C>& acc,
                                            int wm, int wn, int lane, char* slab) const {
@@ -1503,10 +1515,22 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
     const __amdgpu_buffer_rsrc_t rs =
         make_rsrc((kFC1 ? g.dW1 : g.dW2) + (int64_t)e * M(g) * Nn + (int64_t)m0 * Nn,
                   (int64_t)mrows * rowb);
+    const bool add = kDwAddInEpilogue && acc_of(t);
 #pragma clang loop unroll(full)
     for (int mb = 0; mb < C::MB; ++mb) {
       const int r = acc_row<C>(wm, mb, lane);
       const uint32_t ro = r < mrows ? (uint32_t)r * rowb : kOOB;
+      f32x4_t old[C::NB][4];
+      if (add) {
+#pragma clang loop unroll(full)
+        for (int nb = 0; nb < C::NB; ++nb)
+#pragma clang loop unroll(full)
+          for (int gq = 0; gq < 4; ++gq) {
+            const int n = t.n0 + acc_col<C>(wn, nb, gq, lane);
+            old[nb][gq] = __builtin_bit_cast(
+                f32x4_t, load_reg16(rs, n < Nn ? ro + (uint32_t)n * sizeof(float) : kOOB, 0));
+          }
+      }
 #pragma clang loop unroll(full)
       for (int nb = 0; nb < C::NB; ++nb)
 #pragma clang loop unroll(full)
@@ -1514,6 +1538,9 @@ template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
           const int n = t.n0 + acc_col<C>(wn, nb, gq, lane);
           float v[4];
           acc_run(acc.v[mb][nb], gq, v);
+          if (add)
+#pragma clang loop unroll(full)
+            for (int c = 0; c < 4; ++c) v[c] += old[nb][gq][c];
           store_f32x4(rs, n < Nn ? ro + (uint32_t)n * sizeof(float) : kOOB, v);
         }
     }
@@ -1541,8 +1568,9 @@ template <class P, class = void> struct AccLoads { static constexpr bool value =
 template <class P> struct AccLoads<P, decltype((void)P::kAccLoads)> {
   static constexpr bool value = P::kAccLoads;
 };
-// Problems whose epilogue issues a fixed count of vector-memory instructions
-// (P::kEpiStores) can take the deep prefetch below.
+// Problems whose epilogue leaves at most P::kEpiStores vector-memory
+// instructions in flight (its stores; loads it waits for) can take the deep
+// prefetch below.
 template <class P, class = void> struct HasEpiStores { static constexpr bool value = false; };
 template <class P> struct HasEpiStores<P, decltype((void)P::kEpiStores)> {
   static constexpr bool value = true;
@@ -1590,11 +1618,11 @@ constexpr int vm_cap(int n) { return n < 62 ? n : 62; }
 // after the K loop, before the epilogue (with the LDS stages free once it
 // has passed a barrier).
 //
-// `deep` (two-stage direct-copy rings of problems whose epilogue issues a
-// fixed P::kEpiStores vector-memory instructions): the previous tile issued
-// this tile's first two K tiles (issue_prologue2) and then its epilogue, so
-// at K step 0 the copies of K tile 1 and those stores, and at step 1 the
-// stores, were issued after the copies waited for.  Vector-memory
+// `deep` (two-stage direct-copy rings of problems whose epilogue leaves at
+// most P::kEpiStores vector-memory instructions in flight): the previous tile
+// issued this tile's first two K tiles (issue_prologue2) and then its
+// epilogue, so at K step 0 the copies of K tile 1 and those stores, and at
+// step 1 the stores, were issued after the copies waited for.  Vector-memory
 // instructions retire in order, so waiting until only that many are in
 // flight suffices, and the stores drain under the first two K steps.
 template <typename T, class C, class P, int kArray = 0, class Next = NoNext>
