@@ -569,11 +569,15 @@ class ClockSampler:
     """The GPU's current graphics clock (amdsmi), sampled every `period`
     seconds by a daemon thread while the timed steps run.  Everything amdsmi
     does happens on that thread, so a failing or slow query never holds up
-    the measurement; without amdsmi the summary is None."""
+    the measurement; without amdsmi the summary is None.  So it is too when
+    the timed steps take less than `min_seconds`: the reading does not follow
+    short bursts (it stayed at 0.2 GHz through 0.3 s of full load)."""
+
+    min_seconds = 2.0
 
     def __init__(self, period=0.01):
         import threading
-        self.period, self.samples = period, []
+        self.period, self.samples, self.seconds = period, [], 0.0
         self._stop = threading.Event()
         self._thread = threading.Thread(target=self._run, daemon=True)
 
@@ -599,16 +603,20 @@ class ClockSampler:
                 pass
 
     def __enter__(self):
+        import time
+        self._t0 = time.perf_counter()
         self._thread.start()
         return self
 
     def __exit__(self, *exc):
+        import time
+        self.seconds = time.perf_counter() - self._t0
         self._stop.set()
         self._thread.join(timeout=1.0)
 
     def summary(self):
         v = list(self.samples)
-        if not v:
+        if not v or self.seconds < self.min_seconds:
             return None
         return {"mean_ghz": round(sum(v) / len(v) / 1e3, 3), "min_ghz": round(min(v) / 1e3, 3),
                 "max_ghz": round(max(v) / 1e3, 3), "samples": len(v),

@@ -86,11 +86,15 @@ def test_mfma_summary(tmp_path):
 
 
 def test_clock_sampler_summary():
-    """The clock summary: None without samples (no amdsmi, no GPU), else the
-    mean, range and count of the sampled MHz values in GHz."""
+    """The clock summary: None without samples (no amdsmi, no GPU) or over a
+    timed region shorter than the sampler's minimum, else the mean, range
+    and count of the sampled MHz values in GHz."""
     c = bench.ClockSampler()
     assert c.summary() is None
     c.samples = [1800.0, 1700.0, 1600.0]
+    c.seconds = 0.3
+    assert c.summary() is None
+    c.seconds = 5.0
     s = c.summary()
     assert s["mean_ghz"] == pytest.approx(1.7) and s["min_ghz"] == pytest.approx(1.6)
     assert s["max_ghz"] == pytest.approx(1.8) and s["samples"] == 3
