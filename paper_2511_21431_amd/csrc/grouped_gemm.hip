@@ -1277,9 +1277,10 @@ template <typename T, class C> struct ProbFC1Dgrad {
 // kAcc: 1 adds to dW, 0 overwrites it, -1 reads which from GemmArgs (a
 // fixed mode lets the compiler drop the other path's loads and their waits).
 template <typename T, class C, bool kFC1, int kAcc = -1> struct ProbWgrad {
-  static constexpr int kRaster = 0;  // preferred tile order: experts dealt round-robin
+  static constexpr int kRaster = 0;  // preferred tile order: tile ids in order (no XCD blocks)
   static constexpr bool kEqualTiles = false;  // K = the expert's rows
-  static constexpr bool kEpilogueLoads = false;  // the epilogue reads global memory
+  static constexpr bool kEpilogueLoads = false;  // no stage slab; the next tile's copies
+  // go out before the epilogue (its loads of the old dW, when adding, then wait behind them)
   typedef KsOp<T, C::BM, C::NW, C::KB, C::DA> OA;
   typedef KsOp<T, C::BN, C::NW, C::KB, C::DB> OB;
   static constexpr int IG = kFC1 ? OB::I : OA::I;  // copy instructions of the gathered operand
