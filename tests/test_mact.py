@@ -206,6 +206,6 @@ def test_replay_skew_schedule(mf):
 def test_mact_model_I_in_the_gpu_suite(mf):
     """The library's MACT entry points for Model I at every pipeline rank,
     with and without full recomputation, against the oracle (the same check
-    smoke() runs on the GPU machine)."""
+    smoke() runs)."""
     import __graft_entry__ as entry
     entry._smoke_mact(mf)
