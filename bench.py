@@ -285,9 +285,9 @@ def main():
         summarize_counters(args.summarize_counters)
         return
     if args.gpus != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(the expert-parallel exchange is out of scope), so --gpus must be 1",
-              file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU path "
+              "(the expert-parallel exchange between GPUs is not implemented), so --gpus "
+              "must be 1", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -107,3 +107,15 @@ def test_clock_sampler_without_gpu_ends():
     with bench.ClockSampler() as c:
         time.sleep(0.05)
     assert not c._thread.is_alive() or c.summary() is None
+
+
+def test_more_than_one_gpu_is_refused():
+    """bench.py --gpus 2 exits with status 2 and says why, before any GPU
+    work."""
+    import os
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.abspath(bench.__file__), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "exactly one GPU" in r.stderr
